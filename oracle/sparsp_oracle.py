@@ -1,0 +1,366 @@
+"""Plain float64 reference for one rank's share of SparSP sparse attention.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
+benchmark's CPU-baseline leg, never by the product path. Nothing here is
+shared with the HIP library.
+
+The computation follows the paper (arXiv 2609.32197):
+
+* Eq. 1 (Section 2.2): attention O = softmax(Q K^T / sqrt(d)) V.
+* Section 2.2: sparse attention keeps part of the scores and aggregates V
+  with the kept ones; block-sparse kernels renormalise the softmax over the
+  kept keys, which is what this oracle computes.
+* Section 4.1: M[h, i, j] says whether query block i of head h consumes KV
+  block j; Eq. 2 defines a rank's demand as the union of its local rows;
+  Eq. 3 gives the bytes a rank receives.
+* Section 4.2: the mask is built from pooled query and key tiles.
+* Section 5.2: demand is kept per head (not unioned across heads) and blocks
+  are packed row-major, each head a contiguous range, so that offsets can be
+  derived locally on both ends.
+
+Readings taken where the paper is silent (each is listed with its reason in
+the design notes of the repository):
+
+* pooling is the arithmetic mean over the valid tokens of a block;
+* the block score is the pooled dot product scaled by d**-0.5, rounded to
+  float32, with no softmax (softmax is monotone so top-k is unchanged);
+* selection keeps, per row, the diagonal block (global index), the global
+  blocks, and the best remaining blocks by (score descending, index
+  ascending), keep counting every kept block; +0.0 and -0.0 tie; NaN scores
+  are rejected;
+* demand packs every demanded block, local and remote; the remote part is
+  what Eq. 3 counts;
+* the packed K buffer keeps each block as [block, d]; the packed V buffer
+  stores each block transposed, [d, block]; token rows past L are zero.
+
+Precision: every arithmetic step is float64; the float32 block scores are the
+hand-off value for selection. Attention is evaluated directly from Q, K, V
+through the mask (not through the packed buffers) so that it also checks the
+packing and slot map of the GPU path.
+"""
+
+from __future__ import annotations
+
+import math
+from typing import Iterable, Optional, Sequence
+
+import numpy as np
+
+__all__ = [
+    "decode_bf16",
+    "decode_input",
+    "num_blocks",
+    "block_valid_counts",
+    "local_range",
+    "pool_blocks",
+    "block_scores",
+    "forced_blocks",
+    "select_topk",
+    "mask_to_words",
+    "words_to_mask",
+    "demand_union",
+    "packing_plan",
+    "pack_kv",
+    "attend_block",
+    "sparse_attention",
+    "dense_attention",
+    "attention_flops",
+    "exchange_volume",
+]
+
+
+# ---------------------------------------------------------------------------
+# number formats
+# ---------------------------------------------------------------------------
+
+def decode_bf16(bits: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns (uint16) -> float64, exactly.
+
+    A bfloat16 is the upper half of a float32: shift the 16 bits up and
+    reinterpret.
+    """
+    b = np.asarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def decode_input(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Decode a generator tensor ('bf16' bits or 'f32' values) to float64."""
+    if dtype == "bf16":
+        return decode_bf16(x)
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float32).astype(np.float64)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+# ---------------------------------------------------------------------------
+# geometry
+# ---------------------------------------------------------------------------
+
+def num_blocks(L: int, block: int) -> int:
+    """n = ceil(L / b): blocks of b tokens, the last one possibly partial."""
+    return -(-L // block)
+
+
+def block_valid_counts(L: int, block: int) -> np.ndarray:
+    """c_j = min(b, L - j*b): the number of real tokens in block j."""
+    n = num_blocks(L, block)
+    return np.minimum(block, L - block * np.arange(n))
+
+
+def local_range(n: int, ranks: int, rank: int) -> tuple:
+    """Contiguous block ownership: rank r owns [floor(r n / R), floor((r+1) n / R))."""
+    return rank * n // ranks, (rank + 1) * n // ranks
+
+
+# ---------------------------------------------------------------------------
+# Section 4.2: pooled tiles and block scores
+# ---------------------------------------------------------------------------
+
+def pool_blocks(X: np.ndarray, L: int, block: int,
+                blocks: Optional[Iterable[int]] = None) -> np.ndarray:
+    """Mean of each token block over its valid tokens.
+
+    X: float64 [H, L, d]. Returns float64 [H, len(blocks), d] (all n blocks by
+    default). Tokens past L do not exist and are not averaged in.
+    """
+    n = num_blocks(L, block)
+    if blocks is None:
+        blocks = range(n)
+    out = []
+    for j in blocks:
+        lo, hi = j * block, min((j + 1) * block, L)
+        out.append(X[:, lo:hi, :].mean(axis=1))
+    return np.stack(out, axis=1)
+
+
+def block_scores(pooled_q: np.ndarray, pooled_k: np.ndarray, d: int) -> np.ndarray:
+    """S[h, i, j] = <q_bar[h, i], k_bar[h, j]> * d**-0.5, in float64, then rounded to float32."""
+    s = np.matmul(pooled_q, np.swapaxes(pooled_k, 1, 2)) * (1.0 / math.sqrt(d))
+    return s.astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# Section 4.1: the block mask M[h, i, j] by top-k selection
+# ---------------------------------------------------------------------------
+
+def forced_blocks(i: int, global_blocks: Sequence[int]) -> set:
+    """F_i = {i} U G: the diagonal block (global index i) and every global block."""
+    return {int(i)} | {int(g) for g in global_blocks}
+
+
+def select_topk(scores: np.ndarray, keep: int, i0: int,
+                global_blocks: Sequence[int] = ()) -> tuple:
+    """Top-k block selection with a forced diagonal and lowest-index tie-break.
+
+    scores: float32 [H, nq, n]; row r is global query block i = i0 + r.
+    Each row keeps F_i plus the first keep - |F_i| candidates (blocks not in
+    F_i) ordered by score descending, then block index ascending; scores are
+    compared as float32 values, so +0.0 and -0.0 are equal.
+
+    Returns (mask bool [H, nq, n], sel int32 [H, nq, keep] ascending).
+    """
+    s = np.asarray(scores)
+    if s.dtype != np.float32:
+        raise TypeError("scores must be float32")
+    if np.isnan(s).any():
+        raise ValueError("NaN block score")
+    H, nq, n = s.shape
+    G = sorted({int(g) for g in global_blocks})
+    if any(g < 0 or g >= n for g in G):
+        raise ValueError("global block out of range")
+    if keep > n:
+        raise ValueError("keep > n")
+    if i0 < 0 or i0 + nq > n:
+        raise ValueError("local query blocks out of range")
+
+    forced = np.zeros((nq, n), dtype=bool)
+    for r in range(nq):
+        for j in forced_blocks(i0 + r, G):
+            forced[r, j] = True
+    n_forced = forced.sum(axis=1)
+    if (keep < n_forced).any():
+        raise ValueError("keep smaller than the forced set of some row")
+    take = keep - n_forced  # candidates to take per row
+
+    forced3 = np.broadcast_to(forced, (H, nq, n))
+    index = np.broadcast_to(np.arange(n), (H, nq, n))
+    neg_score = -s.astype(np.float64)
+    # lexsort: last key is primary. Candidates first, then score descending,
+    # then index ascending.
+    order = np.lexsort((index, neg_score, forced3), axis=-1)
+    rank = np.empty_like(order)
+    np.put_along_axis(rank, order, np.broadcast_to(np.arange(n), (H, nq, n)), axis=-1)
+    taken = (~forced3) & (rank < take[None, :, None])
+    mask = forced3 | taken
+    sel = np.nonzero(mask)[2].reshape(H, nq, keep).astype(np.int32)
+    return mask, sel
+
+
+def mask_to_words(mask: np.ndarray) -> np.ndarray:
+    """Bit j % 64 of word j // 64 stands for block j. bool [..., n] -> uint64 [..., ceil(n/64)]."""
+    n = mask.shape[-1]
+    W = -(-n // 64)
+    words = np.zeros(mask.shape[:-1] + (W,), dtype=np.uint64)
+    for j in range(n):
+        bit = np.uint64(1) << np.uint64(j % 64)
+        words[..., j // 64] |= np.where(mask[..., j], bit, np.uint64(0))
+    return words
+
+
+def words_to_mask(words: np.ndarray, n: int) -> np.ndarray:
+    """Inverse of mask_to_words."""
+    w = np.asarray(words, dtype=np.uint64)
+    out = np.zeros(w.shape[:-1] + (n,), dtype=bool)
+    for j in range(n):
+        out[..., j] = ((w[..., j // 64] >> np.uint64(j % 64)) & np.uint64(1)) == 1
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Eq. 2 and Section 5.2: per-head demand and the packing plan
+# ---------------------------------------------------------------------------
+
+def demand_union(mask: np.ndarray) -> np.ndarray:
+    """D_h = union over local rows i of {j : M[h, i, j] = 1}, over all owners.
+
+    Demand is kept per head (Section 5.2). mask bool [H, nq, n] -> bool [H, n].
+    """
+    return np.any(mask, axis=1)
+
+
+def packing_plan(demand: np.ndarray) -> tuple:
+    """Row-major packing order: head-major, block index ascending.
+
+    Returns head_off int32 [H+1] (exclusive scan of U_h = |D_h|),
+    gather_blk int32 [sum U_h] (each head's demanded blocks, ascending,
+    heads concatenated) and slot_of int32 [H, n] (slot of block j of head h
+    in the packed buffer, -1 when not demanded).
+    """
+    H, n = demand.shape
+    U = demand.sum(axis=1)
+    head_off = np.zeros(H + 1, dtype=np.int64)
+    head_off[1:] = np.cumsum(U)
+    gather_blk = []
+    slot_of = np.full((H, n), -1, dtype=np.int64)
+    for h in range(H):
+        blocks = np.nonzero(demand[h])[0]
+        gather_blk.extend(blocks.tolist())
+        slot_of[h, blocks] = head_off[h] + np.arange(len(blocks))
+    return (head_off.astype(np.int32), np.asarray(gather_blk, dtype=np.int32),
+            slot_of.astype(np.int32))
+
+
+def pack_kv(K: np.ndarray, V: np.ndarray, head_off: np.ndarray, gather_blk: np.ndarray,
+            L: int, block: int) -> tuple:
+    """Copy the demanded blocks into the packed buffers, bit for bit.
+
+    K, V: raw element arrays [H, L, d] (bf16 bit patterns or float32).
+    Returns K_packed [S, block, d] and V_packed [S, d, block]: slot s holds
+    block gather_blk[s] of its head; the V block is stored transposed; token
+    rows past L are zero.
+    """
+    H, _, d = K.shape
+    S = int(head_off[-1])
+    Kp = np.zeros((S, block, d), dtype=K.dtype)
+    Vp = np.zeros((S, d, block), dtype=V.dtype)
+    for h in range(H):
+        for s in range(int(head_off[h]), int(head_off[h + 1])):
+            j = int(gather_blk[s])
+            lo, hi = j * block, min((j + 1) * block, L)
+            Kp[s, : hi - lo, :] = K[h, lo:hi, :]
+            Vp[s, :, : hi - lo] = V[h, lo:hi, :].T
+    return Kp, Vp
+
+
+# ---------------------------------------------------------------------------
+# Eq. 1 restricted to the kept blocks: block-sparse attention
+# ---------------------------------------------------------------------------
+
+def _softmax_attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float):
+    """Rows of softmax(q k^T * scale) v, with the log-sum-exp of each row."""
+    s = (q @ k.T) * scale
+    m = s.max(axis=1, keepdims=True)
+    e = np.exp(s - m)
+    l = e.sum(axis=1, keepdims=True)
+    return (e @ v) / l, (m + np.log(l))[:, 0], e / l
+
+
+def attend_block(Qh: np.ndarray, Kh: np.ndarray, Vh: np.ndarray, mask_row: np.ndarray,
+                 i: int, L: int, block: int, scale: float, return_probs: bool = False):
+    """Attention of query block i of one head over the valid tokens of its kept blocks.
+
+    Qh, Kh, Vh: float64 [L, d]; mask_row: bool [n]. Returns O [block, d] and
+    lse [block] (natural log); query rows past L get O = 0 and lse = -inf.
+    With return_probs, also the [valid queries, kept tokens] probabilities and
+    the kept token indices.
+    """
+    n = mask_row.shape[0]
+    d = Qh.shape[1]
+    tokens = np.concatenate([np.arange(j * block, min((j + 1) * block, L))
+                             for j in range(n) if mask_row[j]])
+    q_lo, q_hi = i * block, min((i + 1) * block, L)
+    o, lse, p = _softmax_attend(Qh[q_lo:q_hi], Kh[tokens], Vh[tokens], scale)
+    O = np.zeros((block, d))
+    LSE = np.full(block, -np.inf)
+    O[: q_hi - q_lo] = o
+    LSE[: q_hi - q_lo] = lse
+    if return_probs:
+        return O, LSE, p, tokens
+    return O, LSE
+
+
+def sparse_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, mask: np.ndarray,
+                     L: int, block: int, i0: int, scale: float,
+                     pairs: Optional[Iterable[tuple]] = None):
+    """Block-sparse attention of the local query blocks.
+
+    Q, K, V: float64 [H, L, d] (Q may also be given for all tokens; only the
+    local blocks are read). mask: bool [H, nq, n] for rows i0 .. i0+nq-1.
+    Returns O [H, nq*block, d] and lse [H, nq*block]. With ``pairs`` (an
+    iterable of (h, local row) pairs) only those query blocks are evaluated;
+    the rest of O and lse are NaN.
+    """
+    H, nq, n = mask.shape
+    d = Q.shape[2]
+    O = np.full((H, nq * block, d), np.nan)
+    LSE = np.full((H, nq * block), np.nan)
+    if pairs is None:
+        pairs = [(h, r) for h in range(H) for r in range(nq)]
+    for h, r in pairs:
+        o, lse = attend_block(Q[h], K[h], V[h], mask[h, r], i0 + r, L, block, scale)
+        O[h, r * block:(r + 1) * block] = o
+        LSE[h, r * block:(r + 1) * block] = lse
+    return O, LSE
+
+
+def dense_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, scale: float) -> np.ndarray:
+    """Eq. 1 over all tokens of every head: softmax(Q K^T * scale) V."""
+    return np.stack([_softmax_attend(Q[h], K[h], V[h], scale)[0] for h in range(Q.shape[0])])
+
+
+def attention_flops(mask: np.ndarray, L: int, block: int, i0: int, d: int) -> int:
+    """Algorithmic FLOPs of the kept tiles: 4 d c_i c_j per kept (i, j) (QK^T and PV)."""
+    c = block_valid_counts(L, block).astype(np.int64)
+    H, nq, n = mask.shape
+    ci = c[i0:i0 + nq]
+    per_row = mask.astype(np.int64) @ c  # [H, nq]: valid keys per row
+    return int(4 * d * (per_row * ci[None, :]).sum())
+
+
+# ---------------------------------------------------------------------------
+# Eq. 3: bytes received by rank r
+# ---------------------------------------------------------------------------
+
+def exchange_volume(demand: np.ndarray, ranks: int, rank: int, block: int, d: int,
+                    w: int) -> int:
+    """V_r = 2 b d w sum_h sum_{p != r} |D_{r,h,p}| under contiguous ownership.
+
+    Block j is owned by the rank p with floor(p n / R) <= j < floor((p+1) n / R).
+    """
+    H, n = demand.shape
+    owner = np.empty(n, dtype=np.int64)
+    for p in range(ranks):
+        lo, hi = local_range(n, ranks, p)
+        owner[lo:hi] = p
+    remote = demand & (owner[None, :] != rank)
+    return int(2 * block * d * w * remote.sum())
