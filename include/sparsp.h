@@ -1,0 +1,159 @@
+/*
+ * sparsp.h - C ABI of the MI355X (gfx950) library for one rank's share of
+ * SparSP sparse sequence-parallel attention (arXiv 2609.32197).
+ *
+ * The four calls are the four steps of the per-rank hot path:
+ *
+ *   sparsp_block_scores        pool Q and K per token block, score block pairs
+ *                              (Section 4.2: the mask comes from pooled tiles)
+ *   sparsp_topk_mask           block mask M[h,i,j] (Section 4.1) by top-k per
+ *                              query block, diagonal and global blocks forced
+ *   sparsp_demand_union_gather per-head demand union (Eq. 2, Section 5.2) and
+ *                              row-major compaction of the demanded K/V blocks
+ *   sparsp_block_sparse_attn   attention (Eq. 1) of the local query blocks over
+ *                              their kept blocks, read from the packed buffers
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensors are DEVICE pointers owned by the caller. The library allocates
+ *   nothing, keeps no state between calls (except a per-thread error string)
+ *   and never synchronizes: work is enqueued on `stream` (a hipStream_t passed
+ *   as void*, NULL meaning the default stream) and completes in stream order.
+ * - Q, K, V are [H, L, d] row-major with d contiguous, either float32 or
+ *   bfloat16 (geom.dtype). Tokens are cut into n = ceil(L / block) blocks;
+ *   block j covers tokens [j*block, min((j+1)*block, L)).
+ * - The local query blocks are the global block indices [q_blk_begin,
+ *   q_blk_end); nq = q_blk_end - q_blk_begin. W = ceil(n / 64).
+ * - Block masks are bitsets: bit (j % 64) of 64-bit word (j / 64) is block j.
+ * - Every call returns SPARSP_OK (0) or a negative sparsp_status. Argument
+ *   errors are found on the host before anything is launched, so a failing
+ *   call leaves every output untouched. SPARSP_E_HIP reports a launch error;
+ *   sparsp_last_error() gives the message of the calling thread's last error.
+ * - Indices are int32; byte offsets are computed in 64-bit inside the library.
+ * - Limits: n <= 4096 blocks; d <= 256; bf16 attention needs d and block in
+ *   {64, 128}; f32 attention needs d <= 128 and block <= 256; d must be a
+ *   multiple of 8 (bf16) or 4 (f32).
+ */
+#ifndef SPARSP_H
+#define SPARSP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SPARSP_OK = 0,
+    SPARSP_E_INVALID = -1,     /* bad geometry, NULL pointer, out-of-range value */
+    SPARSP_E_DTYPE = -2,       /* unknown or mismatched element type */
+    SPARSP_E_UNSUPPORTED = -3, /* valid but outside the compiled kernel variants */
+    SPARSP_E_CAPACITY = -4,    /* packed buffers smaller than H * n blocks */
+    SPARSP_E_HIP = -5          /* the HIP runtime reported a launch error */
+} sparsp_status;
+
+typedef enum { SPARSP_F32 = 0, SPARSP_BF16 = 1 } sparsp_dtype;
+
+/* Geometry of one rank's share. */
+typedef struct {
+    int32_t H;           /* heads */
+    int32_t L;           /* tokens per head (the whole sequence) */
+    int32_t d;           /* head dimension */
+    int32_t block;       /* tokens per block, b */
+    int32_t q_blk_begin; /* first local query block (global index), i0 */
+    int32_t q_blk_end;   /* one past the last local query block, i1 */
+    int32_t dtype;       /* sparsp_dtype of Q, K, V */
+} sparsp_geom;
+
+/*
+ * Step 1 - pooled tiles and block scores (Section 4.2; mask M of Section 4.1).
+ *
+ *   pooled_q[h,i,:] = mean of Q[h,t,:] over the valid tokens t of block i0+i
+ *   pooled_k[h,j,:] = mean of K[h,t,:] over the valid tokens t of block j
+ *   scores[h,i,j]   = <pooled_q[h,i,:], pooled_k[h,j,:]> * d^-1/2
+ *
+ * Q, K: [H, L, d] in geom.dtype (only the local blocks of Q are read).
+ * pooled_q: float32 [H, nq, d]; pooled_k: float32 [H, n, d]; both are written
+ * (they are outputs, and the working storage of the score step).
+ * scores: float32 [H, nq, n]. Sums are accumulated in float32.
+ */
+int sparsp_block_scores(const sparsp_geom* g, const void* Q, const void* K, float* pooled_q,
+                        float* pooled_k, float* scores, void* stream);
+
+/*
+ * Step 2 - top-k block mask (Section 4.1's M).
+ *
+ * For local row i (global block i0+i) of head h, the forced set is
+ * F = {i0+i} U global_blocks. The row keeps F and the first keep - |F| other
+ * blocks ordered by score descending, then block index ascending. Scores are
+ * compared as float32 values (+0.0 equals -0.0); a NaN score ranks below every
+ * number. `keep` counts every kept block, forced ones included.
+ *
+ * scores: float32 [H, nq, n] device. global_blocks: HOST array of n_global
+ * block indices (may be NULL when n_global == 0; duplicates are ignored;
+ * n_global <= 64). Outputs: mask uint64 [H, nq, W] (bits past n are zero) and
+ * sel int32 [H, nq, keep], each row the kept block indices ascending.
+ * Errors: keep > n, keep < |F| for some row, a global block outside [0, n).
+ * The outputs are a pure function of the score bits.
+ */
+int sparsp_topk_mask(const sparsp_geom* g, const float* scores, int32_t keep,
+                     const int32_t* global_blocks, int32_t n_global, uint64_t* mask,
+                     int32_t* sel, void* stream);
+
+/*
+ * Step 3 - per-head demand union and compaction (Eq. 2 taken over all owners;
+ * Section 5.2: per-head demand, row-major packing, locally derived offsets).
+ *
+ *   demand[h,:]  = OR over local rows i of mask[h,i,:]          uint64 [H, W]
+ *   head_off     = exclusive scan of U_h = popcount(demand[h])  int32 [H+1]
+ *   gather_blk   = each head's demanded blocks ascending, heads
+ *                  concatenated (entries past head_off[H] untouched)
+ *                                                               int32 [capacity]
+ *   slot_of[h,j] = slot of block j of head h, or -1             int32 [H, n]
+ *   K_packed[s]  = K[h, block gather_blk[s]] as [block, d]
+ *   V_packed[s]  = V[h, block gather_blk[s]] TRANSPOSED, as [d, block]
+ *
+ * Token rows past L are zero in both packed buffers. Element type of K, V,
+ * K_packed, V_packed is geom.dtype. capacity_blocks is the number of blocks the
+ * packed buffers and gather_blk can hold; it must be at least H * n so that
+ * the worst case fits without a host round trip (SPARSP_E_CAPACITY otherwise).
+ */
+int sparsp_demand_union_gather(const sparsp_geom* g, const uint64_t* mask, const void* K,
+                               const void* V, uint64_t* demand, int32_t* head_off,
+                               int32_t* slot_of, int32_t* gather_blk, void* K_packed,
+                               void* V_packed, int64_t capacity_blocks, void* stream);
+
+/*
+ * Step 4 - block-sparse attention (Eq. 1 over the kept blocks; the softmax is
+ * renormalised over the kept keys, online, in float32).
+ *
+ * For every valid local query token q of block i0+i, head h:
+ *   T  = valid tokens of the blocks listed in sel[h,i,:]
+ *   O[h, i*block + (q - (i0+i)*block), :] = sum_t softmax_t(Q[h,q]·K[h,t] * scale) V[h,t]
+ *   lse[h, same row] = log sum_t exp(Q[h,q]·K[h,t] * scale)      (natural log)
+ * Query rows past L get O = 0 and lse = -inf.
+ *
+ * Q: [H, L, d] in geom.dtype. sel: int32 [H, nq, keep]. slot_of: int32 [H, n].
+ * K_packed [capacity, block, d] and V_packed [capacity, d, block] as written by
+ * sparsp_demand_union_gather. O: [H, nq*block, d] of out_dtype (F32 always
+ * allowed; BF16, rounded to nearest even, when geom.dtype is BF16).
+ * lse: float32 [H, nq*block] or NULL. A sel entry outside [0, n), or whose
+ * slot is -1 or >= capacity_blocks, is skipped (it contributes nothing).
+ * bf16 inputs use bf16 matrix-core products with float32 accumulation.
+ */
+int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t* sel,
+                             int32_t keep, const int32_t* slot_of, const void* K_packed,
+                             const void* V_packed, int64_t capacity_blocks, float softmax_scale,
+                             void* O, int32_t out_dtype, float* lse, void* stream);
+
+/* Message of the calling thread's most recent error ("" if none). */
+const char* sparsp_last_error(void);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int sparsp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSP_H */

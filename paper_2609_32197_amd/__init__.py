@@ -1,0 +1,305 @@
+"""Python binding of libsparsp: one rank's share of SparSP sparse attention on MI355X.
+
+The four calls mirror the C ABI in include/sparsp.h one to one and only
+marshal arguments: tensors are torch tensors on the GPU (torch provides the
+device memory and the stream), every step of the computation runs in the
+library's HIP kernels. There is no fallback: if the library is not built, or
+a tensor is not on the GPU, the call raises.
+
+    sparsp_block_scores         pooled Q/K tiles and block scores (Section 4.2)
+    sparsp_topk_mask            top-k block mask with forced diagonal (Section 4.1)
+    sparsp_demand_union_gather  per-head demand (Eq. 2) and packed K/V (Section 5.2)
+    sparsp_block_sparse_attn    attention of the local query blocks (Eq. 1)
+
+Short aliases without the prefix are provided as well.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import threading
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+__all__ = [
+    "SparspError",
+    "Geometry",
+    "lib_path",
+    "load_library",
+    "version",
+    "sparsp_block_scores",
+    "sparsp_topk_mask",
+    "sparsp_demand_union_gather",
+    "sparsp_block_sparse_attn",
+    "block_scores",
+    "topk_mask",
+    "demand_union_gather",
+    "block_sparse_attn",
+    "F32",
+    "BF16",
+    "STATUS",
+]
+
+F32, BF16 = 0, 1
+STATUS = {0: "SPARSP_OK", -1: "SPARSP_E_INVALID", -2: "SPARSP_E_DTYPE",
+          -3: "SPARSP_E_UNSUPPORTED", -4: "SPARSP_E_CAPACITY", -5: "SPARSP_E_HIP"}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LOCK = threading.Lock()
+_LIB = None
+
+
+def lib_path() -> str:
+    return os.path.join(_HERE, "libsparsp.so")
+
+
+class SparspError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        self.code = code
+        self.status = STATUS.get(code, str(code))
+        super().__init__(f"{self.status}: {message}")
+
+
+class _Geom(ctypes.Structure):
+    _fields_ = [("H", ctypes.c_int32), ("L", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("block", ctypes.c_int32), ("q_blk_begin", ctypes.c_int32),
+                ("q_blk_end", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+@dataclass(frozen=True)
+class Geometry:
+    """sparsp_geom: Q/K/V are [H, L, d]; local query blocks [i0, i1) of n = ceil(L/block)."""
+
+    H: int
+    L: int
+    d: int
+    block: int
+    i0: int
+    i1: int
+    dtype: int  # F32 or BF16
+
+    @property
+    def n(self) -> int:
+        return -(-self.L // self.block)
+
+    @property
+    def nq(self) -> int:
+        return self.i1 - self.i0
+
+    @property
+    def W(self) -> int:
+        return -(-self.n // 64)
+
+    def c_struct(self) -> _Geom:
+        return _Geom(self.H, self.L, self.d, self.block, self.i0, self.i1, self.dtype)
+
+
+_VP = ctypes.c_void_p
+_SIGNATURES = {
+    "sparsp_block_scores": [ctypes.POINTER(_Geom), _VP, _VP, _VP, _VP, _VP, _VP],
+    "sparsp_topk_mask": [ctypes.POINTER(_Geom), _VP, ctypes.c_int32,
+                         ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, _VP, _VP, _VP],
+    "sparsp_demand_union_gather": [ctypes.POINTER(_Geom), _VP, _VP, _VP, _VP, _VP, _VP, _VP,
+                                   _VP, _VP, ctypes.c_int64, _VP],
+    "sparsp_block_sparse_attn": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP, _VP, _VP,
+                                 ctypes.c_int64, ctypes.c_float, _VP, ctypes.c_int32, _VP, _VP],
+}
+
+
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load libsparsp.so (built in-tree); raises if it is missing."""
+    global _LIB
+    with _LOCK:
+        if _LIB is not None and path is None:
+            return _LIB
+        p = path or lib_path()
+        if not os.path.exists(p):
+            raise RuntimeError(f"{p} is not built: run `python -m paper_2609_32197_amd.build`")
+        lib = ctypes.CDLL(p)
+        for name, args in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = ctypes.c_int
+        lib.sparsp_last_error.argtypes = []
+        lib.sparsp_last_error.restype = ctypes.c_char_p
+        lib.sparsp_version.argtypes = []
+        lib.sparsp_version.restype = ctypes.c_int
+        if path is None:
+            _LIB = lib
+        return lib
+
+
+def version() -> int:
+    return load_library().sparsp_version()
+
+
+def _check(rc: int):
+    if rc != 0:
+        msg = load_library().sparsp_last_error().decode(errors="replace")
+        raise SparspError(rc, msg)
+
+
+# ---------------------------------------------------------------------------
+# tensor marshalling
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _elem_dtype(geom: Geometry):
+    torch = _torch()
+    return torch.bfloat16 if geom.dtype == BF16 else torch.float32
+
+
+def _dev(t, name, dtype=None, shape=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    return t.data_ptr()
+
+
+def _stream(stream, device):
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _empty(shape, dtype, like):
+    return _torch().empty(shape, dtype=dtype, device=like.device)
+
+
+# ---------------------------------------------------------------------------
+# the four calls
+# ---------------------------------------------------------------------------
+
+def sparsp_block_scores(geom: Geometry, Q, K, pooled_q=None, pooled_k=None, scores=None,
+                        stream=None):
+    """Pooled tiles and block scores. Returns (pooled_q [H,nq,d], pooled_k [H,n,d], scores [H,nq,n])."""
+    torch = _torch()
+    g = geom
+    et = _elem_dtype(g)
+    pq = pooled_q if pooled_q is not None else _empty((g.H, g.nq, g.d), torch.float32, Q)
+    pk = pooled_k if pooled_k is not None else _empty((g.H, g.n, g.d), torch.float32, Q)
+    sc = scores if scores is not None else _empty((g.H, g.nq, g.n), torch.float32, Q)
+    args = (
+        _dev(Q, "Q", et, (g.H, g.L, g.d)), _dev(K, "K", et, (g.H, g.L, g.d)),
+        _dev(pq, "pooled_q", torch.float32, (g.H, g.nq, g.d)),
+        _dev(pk, "pooled_k", torch.float32, (g.H, g.n, g.d)),
+        _dev(sc, "scores", torch.float32, (g.H, g.nq, g.n)),
+    )
+    gs = g.c_struct()
+    _check(load_library().sparsp_block_scores(ctypes.byref(gs), *args, _stream(stream, Q.device)))
+    return pq, pk, sc
+
+
+def sparsp_topk_mask(geom: Geometry, scores, keep: int, global_blocks: Sequence[int] = (),
+                     mask=None, sel=None, stream=None):
+    """Top-k block mask. Returns (mask uint64-as-int64 [H,nq,W], sel int32 [H,nq,keep])."""
+    torch = _torch()
+    g = geom
+    m = mask if mask is not None else _empty((g.H, g.nq, g.W), torch.int64, scores)
+    s = sel if sel is not None else _empty((g.H, g.nq, max(int(keep), 0)), torch.int32, scores)
+    gb = list(int(x) for x in global_blocks)
+    arr = (ctypes.c_int32 * max(1, len(gb)))(*gb)
+    args = (
+        _dev(scores, "scores", torch.float32, (g.H, g.nq, g.n)), ctypes.c_int32(int(keep)),
+        arr if gb else None, ctypes.c_int32(len(gb)),
+        _dev(m, "mask", torch.int64, (g.H, g.nq, g.W)),
+        _dev(s, "sel", torch.int32, (g.H, g.nq, max(int(keep), 0))),
+    )
+    gs = g.c_struct()
+    _check(load_library().sparsp_topk_mask(ctypes.byref(gs), *args, _stream(stream, scores.device)))
+    return m, s
+
+
+def sparsp_demand_union_gather(geom: Geometry, mask, K, V, capacity_blocks: Optional[int] = None,
+                               out=None, stream=None):
+    """Per-head demand and packed K/V.
+
+    Returns a dict with demand [H,W] (uint64 bits in int64), head_off [H+1],
+    slot_of [H,n], gather_blk [capacity], K_packed [capacity,block,d] and
+    V_packed [capacity,d,block] (transposed blocks). ``out`` may supply
+    preallocated tensors under the same keys.
+    """
+    torch = _torch()
+    g = geom
+    et = _elem_dtype(g)
+    cap = int(capacity_blocks if capacity_blocks is not None else g.H * g.n)
+    o = dict(out or {})
+    o.setdefault("demand", _empty((g.H, g.W), torch.int64, K))
+    o.setdefault("head_off", _empty((g.H + 1,), torch.int32, K))
+    o.setdefault("slot_of", _empty((g.H, g.n), torch.int32, K))
+    o.setdefault("gather_blk", _empty((cap,), torch.int32, K))
+    o.setdefault("K_packed", _empty((cap, g.block, g.d), et, K))
+    o.setdefault("V_packed", _empty((cap, g.d, g.block), et, K))
+    args = (
+        _dev(mask, "mask", torch.int64, (g.H, g.nq, g.W)),
+        _dev(K, "K", et, (g.H, g.L, g.d)), _dev(V, "V", et, (g.H, g.L, g.d)),
+        _dev(o["demand"], "demand", torch.int64, (g.H, g.W)),
+        _dev(o["head_off"], "head_off", torch.int32, (g.H + 1,)),
+        _dev(o["slot_of"], "slot_of", torch.int32, (g.H, g.n)),
+        _dev(o["gather_blk"], "gather_blk", torch.int32),
+        _dev(o["K_packed"], "K_packed", et), _dev(o["V_packed"], "V_packed", et),
+    )
+    if o["gather_blk"].numel() < cap or o["K_packed"].numel() < cap * g.block * g.d \
+            or o["V_packed"].numel() < cap * g.block * g.d:
+        raise ValueError("output buffers smaller than capacity_blocks")
+    gs = g.c_struct()
+    _check(load_library().sparsp_demand_union_gather(ctypes.byref(gs), *args, ctypes.c_int64(cap),
+                                                    _stream(stream, K.device)))
+    o["capacity_blocks"] = cap
+    return o
+
+
+def sparsp_block_sparse_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed,
+                             softmax_scale: Optional[float] = None, out_dtype: Optional[int] = None,
+                             O=None, lse=None, want_lse: bool = True, stream=None):
+    """Block-sparse attention. Returns (O [H, nq*block, d], lse [H, nq*block] or None)."""
+    torch = _torch()
+    g = geom
+    et = _elem_dtype(g)
+    keep = int(sel.shape[-1])
+    if out_dtype is None:
+        out_dtype = g.dtype
+    odt = torch.bfloat16 if out_dtype == BF16 else torch.float32
+    if softmax_scale is None:
+        softmax_scale = ctypes.c_float(1.0 / math.sqrt(g.d)).value
+    o = O if O is not None else _empty((g.H, g.nq * g.block, g.d), odt, Q)
+    ls = lse if lse is not None else (
+        _empty((g.H, g.nq * g.block), torch.float32, Q) if want_lse else None)
+    if K_packed.dim() != 3 or V_packed.dim() != 3:
+        raise ValueError("K_packed and V_packed must be 3-D")
+    cap = int(K_packed.shape[0])
+    if tuple(K_packed.shape[1:]) != (g.block, g.d) or tuple(V_packed.shape) != (cap, g.d, g.block):
+        raise ValueError("packed buffers must be [cap, block, d] and [cap, d, block]")
+    args = (
+        _dev(Q, "Q", et, (g.H, g.L, g.d)), _dev(sel, "sel", torch.int32, (g.H, g.nq, keep)),
+        ctypes.c_int32(keep), _dev(slot_of, "slot_of", torch.int32, (g.H, g.n)),
+        _dev(K_packed, "K_packed", et), _dev(V_packed, "V_packed", et), ctypes.c_int64(cap),
+        ctypes.c_float(softmax_scale), _dev(o, "O", odt, (g.H, g.nq * g.block, g.d)),
+        ctypes.c_int32(out_dtype),
+        _dev(ls, "lse", torch.float32, (g.H, g.nq * g.block)) if ls is not None else None,
+    )
+    gs = g.c_struct()
+    _check(load_library().sparsp_block_sparse_attn(ctypes.byref(gs), *args,
+                                                  _stream(stream, Q.device)))
+    return o, ls
+
+
+block_scores = sparsp_block_scores
+topk_mask = sparsp_topk_mask
+demand_union_gather = sparsp_demand_union_gather
+block_sparse_attn = sparsp_block_sparse_attn

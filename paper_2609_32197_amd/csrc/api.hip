@@ -1,0 +1,193 @@
+// C ABI of libsparsp: argument checking, geometry derivation and dispatch.
+//
+// Every check runs on the host before any launch, so a call that returns an
+// error has enqueued nothing. The library holds no device state.
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "sparsp_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_err[0] = '\0';
+    return SPARSP_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) e = hipGetLastError();
+    if (e != hipSuccess) return fail(SPARSP_E_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+// Validates the geometry shared by every call and fills `out`.
+int derive(const sparsp_geom* g, sparsp::Geom* out) {
+    if (!g) return fail(SPARSP_E_INVALID, "geom is NULL");
+    if (g->H <= 0 || g->L <= 0 || g->d <= 0 || g->block <= 0)
+        return fail(SPARSP_E_INVALID, "H, L, d and block must be positive (H=%d L=%d d=%d block=%d)",
+                    g->H, g->L, g->d, g->block);
+    if (g->dtype != SPARSP_F32 && g->dtype != SPARSP_BF16)
+        return fail(SPARSP_E_DTYPE, "unknown dtype %d", g->dtype);
+    const int64_t n = (int64_t(g->L) + g->block - 1) / g->block;
+    if (g->q_blk_begin < 0 || g->q_blk_end > n || g->q_blk_begin >= g->q_blk_end)
+        return fail(SPARSP_E_INVALID, "local query blocks [%d, %d) not inside [0, %lld) or empty",
+                    g->q_blk_begin, g->q_blk_end, (long long)n);
+    if (n > sparsp::kMaxBlocks)
+        return fail(SPARSP_E_UNSUPPORTED, "n = %lld blocks exceeds the limit %d", (long long)n,
+                    sparsp::kMaxBlocks);
+    if (g->d > 256) return fail(SPARSP_E_UNSUPPORTED, "d = %d exceeds 256", g->d);
+    const int vec = g->dtype == SPARSP_BF16 ? 8 : 4;
+    if (g->d % vec)
+        return fail(SPARSP_E_UNSUPPORTED, "d = %d must be a multiple of %d for this dtype", g->d, vec);
+    if (int64_t(g->H) * g->L * g->d > (int64_t(1) << 40))
+        return fail(SPARSP_E_INVALID, "H*L*d too large");
+    out->H = g->H;
+    out->L = g->L;
+    out->d = g->d;
+    out->block = g->block;
+    out->i0 = g->q_blk_begin;
+    out->i1 = g->q_blk_end;
+    out->n = int(n);
+    out->nq = g->q_blk_end - g->q_blk_begin;
+    out->W = int((n + 63) / 64);
+    out->bf16 = g->dtype == SPARSP_BF16;
+    return SPARSP_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Packed-block kernels move 16-byte chunks: blocks must hold whole chunks.
+int check_chunked(const sparsp::Geom& G) {
+    const int vec = G.bf16 ? 8 : 4;
+    if (G.block % vec)
+        return fail(SPARSP_E_UNSUPPORTED, "block = %d must be a multiple of %d for this dtype",
+                    G.block, vec);
+    return SPARSP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sparsp_version(void) { return 100; }  // 0.1.0
+
+const char* sparsp_last_error(void) { return g_err; }
+
+int sparsp_block_scores(const sparsp_geom* g, const void* Q, const void* K, float* pooled_q,
+                        float* pooled_k, float* scores, void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!Q || !K || !pooled_q || !pooled_k || !scores)
+        return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (!aligned16(Q) || !aligned16(K))
+        return fail(SPARSP_E_INVALID, "Q and K must be 16-byte aligned");
+    if (G.block > 4096) return fail(SPARSP_E_UNSUPPORTED, "block %d exceeds 4096", G.block);
+    hipError_t e = sparsp::launch_pool_scores(G, Q, K, pooled_q, pooled_k, scores,
+                                              (hipStream_t)stream);
+    return hip_status(e, "sparsp_block_scores");
+}
+
+int sparsp_topk_mask(const sparsp_geom* g, const float* scores, int32_t keep,
+                     const int32_t* global_blocks, int32_t n_global, uint64_t* mask, int32_t* sel,
+                     void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!scores || !mask || !sel) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (n_global < 0 || (n_global > 0 && !global_blocks))
+        return fail(SPARSP_E_INVALID, "global_blocks is NULL but n_global = %d", n_global);
+    if (n_global > sparsp::kMaxGlobal)
+        return fail(SPARSP_E_UNSUPPORTED, "n_global = %d exceeds %d", n_global, sparsp::kMaxGlobal);
+    sparsp::GlobalSet gs;
+    memset(&gs, 0, sizeof(gs));
+    for (int t = 0; t < n_global; ++t) {
+        const int j = global_blocks[t];
+        if (j < 0 || j >= G.n)
+            return fail(SPARSP_E_INVALID, "global block %d outside [0, %d)", j, G.n);
+        gs.w[j >> 6] |= uint64_t(1) << (j & 63);
+    }
+    for (int w = 0; w < sparsp::kMaxWords; ++w) gs.count += __builtin_popcountll(gs.w[w]);
+    if (keep > G.n) return fail(SPARSP_E_INVALID, "keep = %d exceeds n = %d", keep, G.n);
+    // |F_i| = |G| + (i not in G); the largest over local rows bounds keep from below.
+    int max_forced = gs.count;
+    for (int i = G.i0; i < G.i1; ++i)
+        if (!((gs.w[i >> 6] >> (i & 63)) & 1)) { max_forced = gs.count + 1; break; }
+    if (keep < max_forced)
+        return fail(SPARSP_E_INVALID, "keep = %d is smaller than the forced set (%d blocks)", keep,
+                    max_forced);
+    hipError_t e = sparsp::launch_topk(G, scores, keep, gs, mask, sel, (hipStream_t)stream);
+    return hip_status(e, "sparsp_topk_mask");
+}
+
+int sparsp_demand_union_gather(const sparsp_geom* g, const uint64_t* mask, const void* K,
+                               const void* V, uint64_t* demand, int32_t* head_off,
+                               int32_t* slot_of, int32_t* gather_blk, void* K_packed,
+                               void* V_packed, int64_t capacity_blocks, void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!mask || !K || !V || !demand || !head_off || !slot_of || !gather_blk || !K_packed ||
+        !V_packed)
+        return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (G.block > 4096) return fail(SPARSP_E_UNSUPPORTED, "block %d exceeds 4096", G.block);
+    if (int rc = check_chunked(G)) return rc;
+    if (!aligned16(K) || !aligned16(V) || !aligned16(K_packed) || !aligned16(V_packed))
+        return fail(SPARSP_E_INVALID, "K, V and the packed buffers must be 16-byte aligned");
+    const int64_t need = int64_t(G.H) * G.n;
+    if (capacity_blocks < need)
+        return fail(SPARSP_E_CAPACITY, "capacity_blocks = %lld < H*n = %lld",
+                    (long long)capacity_blocks, (long long)need);
+    hipError_t e = sparsp::launch_demand_gather(G, mask, K, V, demand, head_off, slot_of,
+                                                gather_blk, K_packed, V_packed, (hipStream_t)stream);
+    return hip_status(e, "sparsp_demand_union_gather");
+}
+
+int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t keep,
+                             const int32_t* slot_of, const void* K_packed, const void* V_packed,
+                             int64_t capacity_blocks, float softmax_scale, void* O,
+                             int32_t out_dtype, float* lse, void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!Q || !sel || !slot_of || !K_packed || !V_packed || !O)
+        return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (keep < 1 || keep > G.n)
+        return fail(SPARSP_E_INVALID, "keep = %d outside [1, n = %d]", keep, G.n);
+    if (capacity_blocks < 1) return fail(SPARSP_E_CAPACITY, "capacity_blocks < 1");
+    if (int rc = check_chunked(G)) return rc;
+    if (!aligned16(Q) || !aligned16(K_packed) || !aligned16(V_packed) || !aligned16(O))
+        return fail(SPARSP_E_INVALID, "Q, O and the packed buffers must be 16-byte aligned");
+    if (!(softmax_scale > 0.0f) || softmax_scale > 1e30f)
+        return fail(SPARSP_E_INVALID, "softmax_scale must be positive and finite");
+    if (out_dtype != SPARSP_F32 && out_dtype != SPARSP_BF16)
+        return fail(SPARSP_E_DTYPE, "unknown out_dtype %d", out_dtype);
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (G.bf16) {
+        const bool ok_shape = (G.d == 64 || G.d == 128) && (G.block == 64 || G.block == 128);
+        if (!ok_shape)
+            return fail(SPARSP_E_UNSUPPORTED, "bf16 attention needs d and block in {64, 128} (d=%d block=%d)",
+                        G.d, G.block);
+        e = sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                                     softmax_scale, O, out_dtype == SPARSP_BF16, lse, s);
+    } else {
+        if (out_dtype != SPARSP_F32)
+            return fail(SPARSP_E_DTYPE, "f32 inputs produce f32 output only");
+        if (G.d > 128 || G.block > 256)
+            return fail(SPARSP_E_UNSUPPORTED, "f32 attention needs d <= 128 and block <= 256");
+        e = sparsp::launch_attn_f32(G, (const float*)Q, sel, keep, slot_of, (const float*)K_packed,
+                                    (const float*)V_packed, capacity_blocks, softmax_scale,
+                                    (float*)O, lse, s);
+    }
+    return hip_status(e, "sparsp_block_sparse_attn");
+}
+
+}  // extern "C"

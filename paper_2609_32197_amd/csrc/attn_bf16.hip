@@ -1,0 +1,303 @@
+// Step 4, bf16: block-sparse flash attention of the local query blocks over
+// the packed K/V buffers (Eq. 1 over the kept blocks; softmax renormalised
+// over the kept keys, computed online in float32).
+//
+// Work split: one workgroup per (head, local query block), BLK/32 waves, each
+// wave owning 32 query rows. Workgroup ids are remapped so that each of the
+// eight XCDs walks a contiguous range of (head, query block): neighbouring
+// query blocks select overlapping KV blocks, which then hit in that XCD's L2.
+//
+// Per kept KV block the K tile ([BLK, D]) and the transposed V tile ([D, BLK])
+// are staged in LDS with an XOR swizzle of 16-byte chunks, so the MFMA operand
+// reads below are bank-conflict free. The next block's tiles are fetched into
+// registers while the current block is being computed.
+//
+// Products use v_mfma_f32_32x32x16_bf16 with the score tile computed
+// transposed, S^T = K Q^T (A = K from LDS, B = Q^T from registers):
+//   * each lane then holds one query column (q = lane % 32) and 16 keys per
+//     32x32 tile, so the softmax row max and row sum are in-lane except for one
+//     exchange between lanes l and l^32;
+//   * the output is accumulated transposed too, O^T = V^T P^T (A = V^T from
+//     the transposed V tile, B = P^T): the B operand is exactly the lane's own
+//     probabilities converted to bf16, no shuffles. For that to line up, the
+//     lane that feeds A-row m of the K product reads key sigma(m), sigma
+//     swapping bits 2 and 3 of m; then the 8 values a lane holds for each
+//     16-key step of P^T are 8 consecutive keys.
+// MFMA operand layout (32x32x16, wave64): A lane l holds row l%32, k values
+// 8*(l/32) .. +7; B lane l holds column l%32, same k values; the 16 results
+// of lane l are column l%32, rows 8*(r/4) + 4*(l/32) + r%4.
+#include "sparsp_internal.h"
+
+namespace sparsp {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx8 __attribute__((ext_vector_type(8)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ int sigma(int m) {  // swap bits 2 and 3
+    return (m & ~0xC) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+// XOR swizzle of the 16-byte chunk index for a tile whose rows are COLS bf16
+// wide: the 16 rows read together by one quarter-wave land on distinct banks.
+template <int COLS>
+__device__ __forceinline__ int swz(int row) {
+    constexpr int NCH = COLS / 8;                       // chunks per row
+    constexpr int RP = (128 / COLS) > 1 ? 128 / COLS : 1;  // rows per 256 bytes
+    return (row / RP) & (NCH - 1);
+}
+
+// v_permlane32_swap with x in both operands returns, in lane l, the pair
+// {x[l], x[l^32]} in some order; max and sum of the pair are the same in both
+// lanes of the pair, bit for bit.
+__device__ __forceinline__ float pair_max(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int D, int BLK>
+struct Cfg {
+    static constexpr int NW = BLK / 32;           // waves
+    static constexpr int THREADS = 64 * NW;
+    static constexpr int K_CHUNKS = BLK * D / 8;  // 16-byte chunks per tile
+    static constexpr int PER_THREAD = K_CHUNKS / THREADS;
+    static constexpr int MT = BLK / 32;           // key tiles of the score product
+    static constexpr int KT = D / 16;             // k steps of the score product
+    static constexpr int DT = D / 32;             // d tiles of the output product
+    static constexpr int PT = BLK / 16;           // k steps of the output product
+    static_assert(K_CHUNKS % THREADS == 0, "tile must split evenly");
+};
+
+template <int D, int BLK, bool OUT_BF16>
+__global__ __launch_bounds__(2 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict__ sel,
+                      const int32_t* __restrict__ slot_of, const uint16_t* __restrict__ Kp,
+                      const uint16_t* __restrict__ Vp, void* __restrict__ O,
+                      float* __restrict__ lse, int H, int L, int n, int i0, int nq, int keep,
+                      int64_t capacity, float c2 /* scale * log2(e) */, int remap) {
+    using C = Cfg<D, BLK>;
+    __shared__ __attribute__((aligned(16))) uint16_t lds_k[BLK * D];
+    __shared__ __attribute__((aligned(16))) uint16_t lds_v[D * BLK];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int qi = lane & 31, g = lane >> 5;
+
+    // Workgroup -> (head, local query block), XCD-contiguous when remap is on.
+    const int G = H * nq;
+    int wg = blockIdx.x;
+    if (remap) {
+        const int xcd = wg & 7, idx = wg >> 3, per = G >> 3, rem = G & 7;
+        wg = xcd * per + min(xcd, rem) + idx;
+    }
+    const int h = wg / nq, r = wg % nq;
+    const int qtok = (i0 + r) * BLK + wave * 32 + qi;
+    const bool qvalid = qtok < L;
+
+    // Q^T operand: lane holds Q[qtok][16 kt + 8 g .. +7] for every k step.
+    bf16x8 qf[C::KT];
+    {
+        const uint16_t* qp = Q + (int64_t(h) * L + (qvalid ? qtok : 0)) * D + 8 * g;
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt) {
+            uint4 v = qvalid ? *reinterpret_cast<const uint4*>(qp + 16 * kt) : make_uint4(0, 0, 0, 0);
+            qf[kt] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+
+    const int32_t* srow = sel + int64_t(wg) * keep;
+    const int32_t* hslot = slot_of + int64_t(h) * n;
+    auto resolve = [&](int jj, int& slot, int& cnt) {
+        const int j = srow[jj];
+        slot = -1;
+        cnt = 0;
+        if (j >= 0 && j < n) {
+            const int s = hslot[j];
+            if (s >= 0 && s < capacity) {
+                slot = s;
+                cnt = min(BLK, L - j * BLK);
+            }
+        }
+    };
+
+    uint4 kreg[C::PER_THREAD], vreg[C::PER_THREAD];
+    auto fetch = [&](int slot) {
+        const uint4* ks = reinterpret_cast<const uint4*>(Kp + int64_t(slot) * BLK * D);
+        const uint4* vs = reinterpret_cast<const uint4*>(Vp + int64_t(slot) * BLK * D);
+#pragma unroll
+        for (int u = 0; u < C::PER_THREAD; ++u) {
+            kreg[u] = ks[u * C::THREADS + tid];
+            vreg[u] = vs[u * C::THREADS + tid];
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int u = 0; u < C::PER_THREAD; ++u) {
+            const int cid = u * C::THREADS + tid;
+            {
+                const int row = cid / (D / 8), ch = cid % (D / 8);
+                *reinterpret_cast<uint4*>(&lds_k[row * D + ((ch ^ swz<D>(row)) * 8)]) = kreg[u];
+            }
+            {
+                const int row = cid / (BLK / 8), ch = cid % (BLK / 8);
+                *reinterpret_cast<uint4*>(&lds_v[row * BLK + ((ch ^ swz<BLK>(row)) * 8)]) = vreg[u];
+            }
+        }
+    };
+
+    floatx16 oacc[C::DT];
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = floatx16{};
+    float m_run = -INFINITY;  // running max of scaled scores, log2 units
+    float l_run = 0.f;        // this lane's partial row sum
+
+    int slot, cnt;
+    resolve(0, slot, cnt);
+    if (slot >= 0) fetch(slot);
+
+    for (int jj = 0; jj < keep; ++jj) {
+        const int cur_slot = slot, cur_cnt = cnt;
+        __syncthreads();  // every wave is done reading the previous tile
+        if (cur_slot >= 0) stage();
+        __syncthreads();
+        if (jj + 1 < keep) {
+            resolve(jj + 1, slot, cnt);
+            if (slot >= 0) fetch(slot);
+        }
+        if (cur_slot < 0) continue;
+
+        // S^T tile: s[mt][rr] is key 32 mt + 16 (rr/8) + 8 g + rr%8 of query qi.
+        floatx16 s[C::MT];
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt) {
+            floatx16 acc{};
+            const int krow = 32 * mt + sigma(qi);
+            const uint16_t* kr = lds_k + krow * D;
+            const int sw = swz<D>(krow);
+#pragma unroll
+            for (int kt = 0; kt < C::KT; ++kt) {
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(kr + (((2 * kt + g) ^ sw) * 8));
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kt], acc, 0, 0, 0);
+            }
+            s[mt] = acc;
+        }
+        if (cur_cnt < BLK) {
+#pragma unroll
+            for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+                for (int rr = 0; rr < 16; ++rr) {
+                    const int key = 32 * mt + 16 * (rr >> 3) + 8 * g + (rr & 7);
+                    if (key >= cur_cnt) s[mt][rr] = -INFINITY;
+                }
+        }
+
+        float mx = -INFINITY;
+#pragma unroll
+        for (int mt = 0; mt < C::MT; ++mt)
+#pragma unroll
+            for (int rr = 0; rr < 16; ++rr) mx = fmaxf(mx, s[mt][rr]);
+        mx = pair_max(mx);
+        const float m_new = fmaxf(m_run, mx * c2);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
+
+#pragma unroll
+        for (int t = 0; t < C::PT; ++t) {
+            const int mt = t >> 1, hf = t & 1;
+            floatx8 p;
+#pragma unroll
+            for (int v = 0; v < 8; ++v) {
+                p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, -m_new));
+                l_run += p[v];
+            }
+            const bf16x8 pb = __builtin_convertvector(p, bf16x8);
+#pragma unroll
+            for (int dt = 0; dt < C::DT; ++dt) {
+                const int vrow = 32 * dt + qi;
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                    lds_v + vrow * BLK + (((2 * t + g) ^ swz<BLK>(vrow)) * 8));
+                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
+            }
+        }
+    }
+
+    const float l_tot = pair_sum(l_run);
+    const bool live = qvalid && l_tot > 0.f;
+    const float inv = live ? 1.0f / l_tot : 0.f;
+    const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + wave * 32 + qi;
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const int d0 = 32 * dt + 8 * q4 + 4 * g;
+            float o4[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) o4[u] = oacc[dt][4 * q4 + u] * inv;
+            if constexpr (OUT_BF16) {
+                uint16_t* op = static_cast<uint16_t*>(O) + orow * D + d0;
+                uint2 w;
+                w.x = f32_to_bf16_bits(o4[0]) | (f32_to_bf16_bits(o4[1]) << 16);
+                w.y = f32_to_bf16_bits(o4[2]) | (f32_to_bf16_bits(o4[3]) << 16);
+                *reinterpret_cast<uint2*>(op) = w;
+            } else {
+                float* op = static_cast<float*>(O) + orow * D + d0;
+                *reinterpret_cast<float4*>(op) = make_float4(o4[0], o4[1], o4[2], o4[3]);
+            }
+        }
+    }
+    if (lse && g == 0) lse[orow] = live ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+}
+
+template <int D, int BLK>
+hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int keep,
+                        const int32_t* slot_of, const void* Kp, const void* Vp, int64_t cap,
+                        float scale, void* O, bool out_bf16, float* lse, hipStream_t s) {
+    using C = Cfg<D, BLK>;
+    const int G = g.H * g.nq;
+    const float c2 = scale * kLog2e;
+    const int remap = 1;
+    if (out_bf16)
+        attn_bf16_kernel<D, BLK, true><<<G, C::THREADS, 0, s>>>(
+            (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
+            g.H, g.L, g.n, g.i0, g.nq, keep, cap, c2, remap);
+    else
+        attn_bf16_kernel<D, BLK, false><<<G, C::THREADS, 0, s>>>(
+            (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
+            g.H, g.L, g.n, g.i0, g.nq, keep, cap, c2, remap);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, int keep,
+                            const int32_t* slot_of, const void* Kp, const void* Vp,
+                            int64_t capacity, float scale, void* O, bool out_bf16, float* lse,
+                            hipStream_t s) {
+    (void)hipGetLastError();
+    if (g.d == 128 && g.block == 128)
+        return launch_shape<128, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, O,
+                                      out_bf16, lse, s);
+    if (g.d == 64 && g.block == 64)
+        return launch_shape<64, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, O,
+                                    out_bf16, lse, s);
+    if (g.d == 128 && g.block == 64)
+        return launch_shape<128, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, O,
+                                     out_bf16, lse, s);
+    if (g.d == 64 && g.block == 128)
+        return launch_shape<64, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, O,
+                                     out_bf16, lse, s);
+    return hipErrorInvalidValue;
+}
+
+}  // namespace sparsp

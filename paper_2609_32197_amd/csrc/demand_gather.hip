@@ -1,0 +1,203 @@
+// Step 3: per-head demand union (Eq. 2 over all owners, kept per head as
+// Section 5.2 requires) and row-major compaction of the demanded blocks.
+//
+// union_kernel   one workgroup per head: OR of the nq mask rows, word-parallel.
+// offsets_kernel one workgroup per head: head_off[h] is the popcount of all
+//                earlier heads' demand words (integer sums, so exact and
+//                deterministic without a cross-workgroup scan); then every
+//                block's slot = head_off[h] + rank of the block in D_h, which
+//                fills slot_of and gather_blk. Both ends of an exchange could
+//                derive these offsets locally from the same bitsets.
+// gather_kernel  one workgroup per (block, head); blocks that are not demanded
+//                exit at once. K blocks are copied with 16-byte loads and
+//                stores; V blocks are written transposed ([d, block]) so the
+//                attention kernel reads V^T MFMA operands with contiguous
+//                16-byte loads. Each thread moves a VEC x VEC sub-block and
+//                transposes it in registers. Rows past L are written as zero.
+//                The grid covers all H*n blocks, so no host round trip is
+//                needed to learn the demand total.
+#include "sparsp_internal.h"
+
+namespace sparsp {
+namespace {
+
+__global__ __launch_bounds__(256) void union_kernel(const uint64_t* __restrict__ mask, int nq,
+                                                    int W, uint64_t* __restrict__ demand) {
+    __shared__ uint64_t part[4][64];
+    const int h = blockIdx.x;
+    const int w = threadIdx.x & 63;
+    const int rg = threadIdx.x >> 6;
+    uint64_t acc = 0;
+    if (w < W) {
+        const uint64_t* m = mask + int64_t(h) * nq * W + w;
+        for (int i = rg; i < nq; i += 4) acc |= m[int64_t(i) * W];
+    }
+    part[rg][w] = acc;
+    __syncthreads();
+    if (rg == 0 && w < W) demand[int64_t(h) * W + w] = part[0][w] | part[1][w] | part[2][w] | part[3][w];
+}
+
+__global__ __launch_bounds__(256) void offsets_kernel(const uint64_t* __restrict__ demand, int H,
+                                                      int n, int W, int32_t* __restrict__ head_off,
+                                                      int32_t* __restrict__ slot_of,
+                                                      int32_t* __restrict__ gather_blk) {
+    __shared__ int red[256];
+    __shared__ int word_prefix[kMaxWords];
+    const int h = blockIdx.x;
+    const int tid = threadIdx.x;
+
+    // Demanded blocks of all earlier heads.
+    int c = 0;
+    for (int e = tid; e < h * W; e += 256) c += __popcll(demand[e]);
+    red[tid] = c;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if (tid < s) red[tid] += red[tid + s];
+        __syncthreads();
+    }
+    const int prefix = red[0];
+    const uint64_t* dh = demand + int64_t(h) * W;
+    if (tid == 0) {
+        int run = 0;
+        for (int w = 0; w < W; ++w) {
+            word_prefix[w] = run;
+            run += __popcll(dh[w]);
+        }
+        head_off[h] = prefix;
+        if (h == H - 1) head_off[H] = prefix + run;
+    }
+    __syncthreads();
+    for (int j = tid; j < n; j += 256) {
+        const uint64_t word = dh[j >> 6];
+        const int bit = j & 63;
+        int32_t slot = -1;
+        if ((word >> bit) & 1) {
+            const uint64_t below = bit ? (word & ((uint64_t(1) << bit) - 1)) : 0;
+            slot = prefix + word_prefix[j >> 6] + __popcll(below);
+            gather_blk[slot] = j;
+        }
+        slot_of[int64_t(h) * n + j] = slot;
+    }
+}
+
+// 16-bit transpose of an 8x8 tile held as 8 rows of uint4: out[c] holds column c.
+__device__ __forceinline__ void transpose8x8_b16(const uint4 (&in)[8], uint4 (&out)[8]) {
+    uint32_t a[8][4];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+        a[r][0] = in[r].x; a[r][1] = in[r].y; a[r][2] = in[r].z; a[r][3] = in[r].w;
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        uint32_t o[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            // element (row 2p, col c) -> low half; (row 2p+1, col c) -> high half
+            const uint32_t lo = (a[2 * p][c >> 1] >> ((c & 1) * 16)) & 0xffffu;
+            const uint32_t hi = (a[2 * p + 1][c >> 1] >> ((c & 1) * 16)) & 0xffffu;
+            o[p] = lo | (hi << 16);
+        }
+        out[c] = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+}
+
+__device__ __forceinline__ void transpose4x4_b32(const uint4 (&in)[4], uint4 (&out)[4]) {
+    out[0] = make_uint4(in[0].x, in[1].x, in[2].x, in[3].x);
+    out[1] = make_uint4(in[0].y, in[1].y, in[2].y, in[3].y);
+    out[2] = make_uint4(in[0].z, in[1].z, in[2].z, in[3].z);
+    out[3] = make_uint4(in[0].w, in[1].w, in[2].w, in[3].w);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__ slot_of,
+                                                     const char* __restrict__ K,
+                                                     const char* __restrict__ V,
+                                                     char* __restrict__ Kp, char* __restrict__ Vp,
+                                                     int L, int d, int block, int n) {
+    constexpr int ES = BF16 ? 2 : 4;     // element size
+    constexpr int VEC = 16 / ES;         // elements per 16-byte chunk
+    const int j = blockIdx.x;
+    const int h = blockIdx.y;
+    const int slot = slot_of[int64_t(h) * n + j];
+    if (slot < 0) return;
+    const int tid = threadIdx.x;
+    const int tok0 = j * block;
+    const int cnt = min(block, L - tok0);
+    const int64_t blk_bytes = int64_t(block) * d * ES;
+    const char* ksrc = K + (int64_t(h) * L + tok0) * d * ES;
+    const char* vsrc = V + (int64_t(h) * L + tok0) * d * ES;
+    char* kdst = Kp + int64_t(slot) * blk_bytes;
+    char* vdst = Vp + int64_t(slot) * blk_bytes;
+
+    // K: straight copy of `cnt` rows, zero rows after.
+    const int row_chunks = d / VEC;
+    const int total = block * row_chunks;
+    const int valid = cnt * row_chunks;
+    for (int e = tid; e < total; e += 256) {
+        uint4 x = make_uint4(0, 0, 0, 0);
+        if (e < valid) x = *reinterpret_cast<const uint4*>(ksrc + int64_t(e) * 16);
+        *reinterpret_cast<uint4*>(kdst + int64_t(e) * 16) = x;
+    }
+
+    // V: transposed copy by VEC x VEC sub-blocks. Sub-block (kb, db) covers tokens
+    // kb*VEC .. +VEC-1 and dims db*VEC .. +VEC-1. Consecutive threads take
+    // consecutive db, so each load instruction reads whole token rows.
+    const int dblocks = d / VEC;
+    const int kblocks = (block + VEC - 1) / VEC;
+    for (int e = tid; e < dblocks * kblocks; e += 256) {
+        const int db = e % dblocks, kb = e / dblocks;
+        uint4 rows[VEC], cols[VEC];
+#pragma unroll
+        for (int r = 0; r < VEC; ++r) {
+            const int t = kb * VEC + r;
+            rows[r] = make_uint4(0, 0, 0, 0);
+            if (t < cnt)
+                rows[r] = *reinterpret_cast<const uint4*>(vsrc + (int64_t(t) * d + db * VEC) * ES);
+        }
+        if constexpr (BF16) transpose8x8_b16(rows, cols);
+        else transpose4x4_b32(rows, cols);
+        // cols[c] = dim db*VEC+c, tokens kb*VEC .. +VEC-1 -> Vp[slot][dim][token]
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+            const int64_t off = (int64_t(db * VEC + c) * block + kb * VEC) * ES;
+            if (kb * VEC + VEC <= block) {
+                *reinterpret_cast<uint4*>(vdst + off) = cols[c];
+            } else {
+                // Ragged block size: store the in-range elements one by one.
+                const uint32_t w[4] = {cols[c].x, cols[c].y, cols[c].z, cols[c].w};
+                for (int u = 0; u < VEC && kb * VEC + u < block; ++u) {
+                    if constexpr (BF16) {
+                        const uint16_t v16 = uint16_t((w[u >> 1] >> ((u & 1) * 16)) & 0xffffu);
+                        *reinterpret_cast<uint16_t*>(vdst + off + u * 2) = v16;
+                    } else {
+                        *reinterpret_cast<uint32_t*>(vdst + off + u * 4) = w[u];
+                    }
+                }
+            }
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void* K, const void* V,
+                                uint64_t* demand, int32_t* head_off, int32_t* slot_of,
+                                int32_t* gather_blk, void* Kp, void* Vp, hipStream_t s) {
+    (void)hipGetLastError();
+    union_kernel<<<g.H, 256, 0, s>>>(mask, g.nq, g.W, demand);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    offsets_kernel<<<g.H, 256, 0, s>>>(demand, g.H, g.n, g.W, head_off, slot_of, gather_blk);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 grid(g.n, g.H);
+    if (g.bf16)
+        gather_kernel<true><<<grid, 256, 0, s>>>(slot_of, (const char*)K, (const char*)V, (char*)Kp,
+                                                 (char*)Vp, g.L, g.d, g.block, g.n);
+    else
+        gather_kernel<false><<<grid, 256, 0, s>>>(slot_of, (const char*)K, (const char*)V,
+                                                  (char*)Kp, (char*)Vp, g.L, g.d, g.block, g.n);
+    return hipGetLastError();
+}
+
+}  // namespace sparsp

@@ -1,0 +1,64 @@
+// Internal declarations shared by the HIP translation units of libsparsp.
+// Kernels are launched only through these functions; argument checking has
+// already happened in api.hip when they are called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sparsp.h"
+
+namespace sparsp {
+
+constexpr int kMaxBlocks = 4096;        // n limit: 64 mask words per row
+constexpr int kMaxWords = kMaxBlocks / 64;
+constexpr int kMaxGlobal = 64;          // global (always-kept) blocks per call
+
+// Derived geometry, computed once on the host.
+struct Geom {
+    int H, L, d, block, i0, i1, n, nq, W;
+    bool bf16;
+};
+
+// Forced global blocks as a bitset, passed by value as a kernel argument.
+struct GlobalSet {
+    uint64_t w[kMaxWords];
+    int count;  // distinct global blocks
+};
+
+hipError_t launch_pool_scores(const Geom& g, const void* Q, const void* K, float* pooled_q,
+                              float* pooled_k, float* scores, hipStream_t s);
+
+hipError_t launch_topk(const Geom& g, const float* scores, int keep, const GlobalSet& gs,
+                       uint64_t* mask, int32_t* sel, hipStream_t s);
+
+hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void* K, const void* V,
+                                uint64_t* demand, int32_t* head_off, int32_t* slot_of,
+                                int32_t* gather_blk, void* Kp, void* Vp, hipStream_t s);
+
+hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, int keep,
+                            const int32_t* slot_of, const void* Kp, const void* Vp,
+                            int64_t capacity, float scale, void* O, bool out_bf16, float* lse,
+                            hipStream_t s);
+
+hipError_t launch_attn_f32(const Geom& g, const float* Q, const int32_t* sel, int keep,
+                           const int32_t* slot_of, const float* Kp, const float* Vp,
+                           int64_t capacity, float scale, float* O, float* lse, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// device helpers
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+
+// float32 -> bfloat16 bits, round to nearest even (finite inputs; NaN kept quiet).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float x) {
+    uint32_t u = __float_as_uint(x);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+}  // namespace sparsp

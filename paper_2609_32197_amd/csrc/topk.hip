@@ -1,0 +1,121 @@
+// Step 2: top-k block mask (Section 4.1's M) with the diagonal and global
+// blocks forced and ties broken by the lower block index.
+//
+// One wave64 per (head, local row). Lane l holds blocks j = l + 64 s
+// (s = 0 .. S-1) in registers, so the 64 lanes of chunk s are exactly the 64
+// bits of mask word s: a ballot builds a mask word directly.
+//
+// Selection is exact and order-free. Scores become order-preserving 32-bit
+// keys (-0.0 folded onto +0.0, NaN below every number). A 32-step bitwise
+// search finds T, the k-th largest candidate key (k = keep - |F|): at each bit
+// it keeps the bit set if at least k candidates still reach the threshold.
+// Candidates above T are taken; among those equal to T the lowest indices are
+// taken until k is reached, ranked in index order with ballots and
+// mbcnt. No floating point is involved, so the result is a pure function of
+// the score bits.
+#include "sparsp_internal.h"
+
+namespace sparsp {
+namespace {
+
+__device__ __forceinline__ uint32_t order_key(float x) {
+    uint32_t u = __float_as_uint(x);
+    if (u == 0x80000000u) u = 0u;                                   // -0.0 ties +0.0
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0u;  // NaN: lowest
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ int popc64(uint64_t x) { return __popcll(x); }
+
+// Number of set bits of `b` below this lane.
+__device__ __forceinline__ int below_lane(uint64_t b) {
+    return __builtin_amdgcn_mbcnt_hi(uint32_t(b >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(b), 0));
+}
+
+template <int S>
+__global__ __launch_bounds__(256) void topk_kernel(const float* __restrict__ scores, int H, int nq,
+                                                   int n, int W, int i0, int keep, GlobalSet gs,
+                                                   uint64_t* __restrict__ mask,
+                                                   int32_t* __restrict__ sel) {
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);  // h * nq + r
+    if (row >= H * nq) return;  // whole wave exits together
+    const int r = row % nq;
+    const int i = i0 + r;  // global index of this query block: the forced diagonal
+
+    const float* srow = scores + int64_t(row) * n;
+    uint32_t key[S];
+    bool cand[S], forced[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const int j = lane + 64 * s;
+        const bool valid = j < n;
+        const bool f = valid && (j == i || ((gs.w[s] >> lane) & 1));
+        forced[s] = f;
+        cand[s] = valid && !f;
+        key[s] = valid ? order_key(srow[j]) : 0u;
+    }
+    const bool diag_in_g = (gs.w[i >> 6] >> (i & 63)) & 1;
+    const int n_forced = gs.count + (diag_in_g ? 0 : 1);
+    const int k = keep - n_forced;  // candidates to take, >= 0 (checked on the host)
+
+    uint32_t T = 0;
+    int need = 0;  // how many candidates equal to T to take
+    if (k > 0) {
+        for (int b = 31; b >= 0; --b) {
+            const uint32_t t = T | (1u << b);
+            int cnt = 0;
+#pragma unroll
+            for (int s = 0; s < S; ++s) cnt += popc64(__ballot(cand[s] && key[s] >= t));
+            if (cnt >= k) T = t;
+        }
+        int gt = 0;
+#pragma unroll
+        for (int s = 0; s < S; ++s) gt += popc64(__ballot(cand[s] && key[s] > T));
+        need = k - gt;  // >= 1 by the choice of T
+    }
+
+    uint64_t* mrow = mask + int64_t(row) * W;
+    int32_t* selrow = sel + int64_t(row) * keep;
+    int ties_seen = 0, written = 0;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        bool take = forced[s];
+        if (k > 0) {
+            const bool eq = cand[s] && key[s] == T;
+            const uint64_t eqb = __ballot(eq);
+            const bool take_eq = eq && (ties_seen + below_lane(eqb)) < need;
+            ties_seen += popc64(eqb);
+            take = take || (cand[s] && key[s] > T) || take_eq;
+        }
+        const uint64_t word = __ballot(take);
+        if (s < W && lane == 0) mrow[s] = word;
+        if (take) selrow[written + below_lane(word)] = lane + 64 * s;
+        written += popc64(word);
+    }
+}
+
+template <int S>
+hipError_t launch_s(const Geom& g, const float* scores, int keep, const GlobalSet& gs,
+                    uint64_t* mask, int32_t* sel, hipStream_t st) {
+    const int rows = g.H * g.nq;
+    topk_kernel<S><<<(rows + 3) / 4, 256, 0, st>>>(scores, g.H, g.nq, g.n, g.W, g.i0, keep, gs,
+                                                   mask, sel);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_topk(const Geom& g, const float* scores, int keep, const GlobalSet& gs,
+                       uint64_t* mask, int32_t* sel, hipStream_t st) {
+    (void)hipGetLastError();
+    if (g.W <= 1) return launch_s<1>(g, scores, keep, gs, mask, sel, st);
+    if (g.W <= 2) return launch_s<2>(g, scores, keep, gs, mask, sel, st);
+    if (g.W <= 4) return launch_s<4>(g, scores, keep, gs, mask, sel, st);
+    if (g.W <= 8) return launch_s<8>(g, scores, keep, gs, mask, sel, st);
+    if (g.W <= 16) return launch_s<16>(g, scores, keep, gs, mask, sel, st);
+    if (g.W <= 32) return launch_s<32>(g, scores, keep, gs, mask, sel, st);
+    return launch_s<64>(g, scores, keep, gs, mask, sel, st);
+}
+
+}  // namespace sparsp
