@@ -1,0 +1,302 @@
+#!/usr/bin/env python3
+"""Benchmark of one rank's share of SparSP sparse attention on one MI355X.
+
+One step is the whole per-rank hot path over one batch of synthetic input
+already resident in HBM: pooled scores -> top-k mask -> demand union and
+compaction -> block-sparse attention, the four calls of libsparsp.
+
+    python bench.py [--steps K] [--warmup W] [--workload wan-share]
+
+Prints ONE JSON line on stdout. `value` is the whole step's throughput in
+TFLOP/s of algorithmic attention work over the kept (unmasked) tiles,
+4 * d * c_i * c_j FLOPs per kept (query block i, KV block j) pair with c the
+valid token counts; `ms_per_step` is the layer time. The `roofline` object
+is for the dominant kernel (attention), timed with HIP events on the stream
+it runs on. `cpu_baseline` is the float64 oracle timed on a bounded sample of
+the same workload on the host cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "block-sparse attn ms/layer + TFLOP/s on unmasked tiles (% MFMA peak), 1 GPU"
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3    # MI355X fp32 (vector / matrix)
+PEAK_HBM_GBPS = 8000.0     # MI355X HBM3E
+ATTN_SRC = os.path.join(ROOT, "paper_2609_32197_amd", "csrc", "attn_bf16.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "attn_bf16_wan-share_counters.md")
+
+
+def parse_args(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="wan-share")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="wall-clock budget of the oracle sample")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of this many MiB (for counter calibration)")
+    return ap.parse_args(argv)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def copy_calibration(mib: int):
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copied {mib} MiB x 5")
+
+
+def file_sha(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def read_traffic():
+    """HBM bytes per attention launch from the committed counter summary, if current."""
+    if not os.path.exists(COUNTERS):
+        return None, "no counter summary"
+    text = open(COUNTERS).read()
+    m_sha = re.search(r"source sha256\[:16\]:\s*`?([0-9a-f]{16})", text)
+    m_b = re.search(r"HBM bytes per launch \(calibrated\):\s*([0-9.eE+]+)", text)
+    if not m_sha or not m_b:
+        return None, "counter summary unreadable"
+    if m_sha.group(1) != file_sha(ATTN_SRC):
+        return None, "kernel changed since the counters were taken"
+    return float(m_b.group(1)), "ok"
+
+
+def attention_flops(sel, L, block, i0, d):
+    import numpy as np
+    n = -(-L // block)
+    c = np.minimum(block, L - block * np.arange(n)).astype(np.int64)
+    H, nq, keep = sel.shape
+    kv = c[sel].sum(axis=2)                       # valid keys per row
+    ci = c[i0:i0 + nq]
+    return int(4 * d * (kv * ci[None, :]).sum())
+
+
+def gather_bytes(slot_of, L, block, d, w):
+    """Algorithmic bytes of the compaction: read valid K and V rows, write whole packed blocks."""
+    import numpy as np
+    n = -(-L // block)
+    c = np.minimum(block, L - block * np.arange(n)).astype(np.int64)
+    dem = slot_of >= 0
+    reads = int((dem * c[None, :]).sum()) * 2 * d * w
+    writes = int(dem.sum()) * 2 * block * d * w
+    return reads + writes + slot_of.size * 4
+
+
+def cpu_baseline(wl, q, k, v, budget_s):
+    """Time the float64 oracle over whole heads of the same workload until the budget is spent."""
+    import numpy as np
+    import oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # threadpoolctl missing: numpy's default pool
+        threads = os.cpu_count() or 1
+    flops = 0
+    spent = 0.0
+    heads = 0
+    for h in range(wl.H):
+        t0 = time.perf_counter()
+        Qh, Kh, Vh = (orc.decode_input(x[h:h + 1], wl.dtype) for x in (q, k, v))
+        pq = orc.pool_blocks(Qh, wl.L, wl.block, range(wl.i0, wl.i1))
+        pk = orc.pool_blocks(Kh, wl.L, wl.block)
+        s = orc.block_scores(pq, pk, wl.d)
+        mask, _ = orc.select_topk(s, wl.keep, wl.i0, wl.global_blocks)
+        D = orc.demand_union(mask)
+        head_off, gather_blk, _ = orc.packing_plan(D)
+        orc.pack_kv(k[h:h + 1], v[h:h + 1], head_off, gather_blk, wl.L, wl.block)
+        orc.sparse_attention(Qh, Kh, Vh, mask, wl.L, wl.block, wl.i0, wl.softmax_scale)
+        spent += time.perf_counter() - t0
+        flops += orc.attention_flops(mask, wl.L, wl.block, wl.i0, wl.d)
+        heads += 1
+        if spent >= budget_s:
+            break
+    return {
+        "value": flops / spent / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{heads} of {wl.H} heads, whole pipeline (pool, score, select, union, pack, "
+                  f"attend) per head, {spent:.1f} s",
+    }
+
+
+def main(argv=None) -> int:
+    a = parse_args(argv)
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if a.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs one rank's share on ONE GPU; "
+                                   f"--gpus {a.gpus} (WORLD_SIZE={world}) is not supported",
+                          "n_gpus": a.gpus}))
+        return 2
+
+    import numpy as np
+    import torch
+
+    if a.copy_calibration:
+        copy_calibration(a.copy_calibration)
+        return 0
+
+    import paper_2609_32197_amd as sp
+    from workloads import get_workload, make_qkv
+
+    wl = get_workload(a.workload)
+    t0 = time.time()
+    q, k, v = make_qkv(wl, seed=a.seed)
+    log(f"[bench] generated {wl.name} inputs in {time.time() - t0:.1f}s")
+
+    def dev(x):
+        if wl.dtype == "bf16":
+            return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(x).cuda()
+
+    Q, K, V = dev(q), dev(k), dev(v)
+    g = sp.Geometry(wl.H, wl.L, wl.d, wl.block, wl.i0, wl.i1,
+                    sp.BF16 if wl.dtype == "bf16" else sp.F32)
+    f32, i32, i64 = torch.float32, torch.int32, torch.int64
+    cap = wl.H * wl.n
+    et = Q.dtype
+    bufs = dict(
+        pooled_q=torch.empty((wl.H, wl.nq, wl.d), dtype=f32, device="cuda"),
+        pooled_k=torch.empty((wl.H, wl.n, wl.d), dtype=f32, device="cuda"),
+        scores=torch.empty((wl.H, wl.nq, wl.n), dtype=f32, device="cuda"),
+        mask=torch.empty((wl.H, wl.nq, g.W), dtype=i64, device="cuda"),
+        sel=torch.empty((wl.H, wl.nq, wl.keep), dtype=i32, device="cuda"),
+        O=torch.empty((wl.H, wl.nq * wl.block, wl.d), dtype=et, device="cuda"),
+        lse=torch.empty((wl.H, wl.nq * wl.block), dtype=f32, device="cuda"),
+    )
+    packed = dict(
+        demand=torch.empty((wl.H, g.W), dtype=i64, device="cuda"),
+        head_off=torch.empty((wl.H + 1,), dtype=i32, device="cuda"),
+        slot_of=torch.empty((wl.H, wl.n), dtype=i32, device="cuda"),
+        gather_blk=torch.empty((cap,), dtype=i32, device="cuda"),
+        K_packed=torch.empty((cap, wl.block, wl.d), dtype=et, device="cuda"),
+        V_packed=torch.empty((cap, wl.d, wl.block), dtype=et, device="cuda"),
+    )
+    out_dtype = sp.BF16 if wl.dtype == "bf16" else sp.F32
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        sp.sparsp_block_scores(g, Q, K, bufs["pooled_q"], bufs["pooled_k"], bufs["scores"],
+                               stream=stream)
+        if ev: ev[1].record(stream)
+        sp.sparsp_topk_mask(g, bufs["scores"], wl.keep, wl.global_blocks, bufs["mask"],
+                            bufs["sel"], stream=stream)
+        if ev: ev[2].record(stream)
+        sp.sparsp_demand_union_gather(g, bufs["mask"], K, V, cap, out=packed, stream=stream)
+        if ev: ev[3].record(stream)
+        sp.sparsp_block_sparse_attn(g, Q, bufs["sel"], packed["slot_of"], packed["K_packed"],
+                                    packed["V_packed"], wl.softmax_scale, out_dtype=out_dtype,
+                                    O=bufs["O"], lse=bufs["lse"], stream=stream)
+        if ev: ev[4].record(stream)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # Timed region: K steps back to back, per-stage HIP events on the same stream.
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(a.steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for s in range(a.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3 / a.steps
+    stage_names = ["block_scores", "topk_mask", "demand_union_gather", "block_sparse_attn"]
+    stage_ms = {nm: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(a.steps)]))
+                for i, nm in enumerate(stage_names)}
+    ms_per_step = float(np.mean([evs[s][0].elapsed_time(evs[s][4]) for s in range(a.steps)]))
+
+    sel = bufs["sel"].cpu().numpy()
+    slot_of = packed["slot_of"].cpu().numpy()
+    flops = attention_flops(sel, wl.L, wl.block, wl.i0, wl.d)
+    gbytes = gather_bytes(slot_of, wl.L, wl.block, wl.d, wl.bytes_per_elem)
+    attn_tflops = flops / (stage_ms["block_sparse_attn"] * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    demanded = int((slot_of >= 0).sum())
+    traffic, traffic_note = read_traffic() if wl.name == "wan-share" else (None, "other workload")
+
+    rec = {
+        "metric": METRIC,
+        "value": flops / (ms_per_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded generator standing in for the paper's video-DiT activations)",
+        "config": {
+            "workload": wl.name, "H": wl.H, "d": wl.d, "block": wl.block, "L": wl.L,
+            "n_blocks": wl.n, "local_blocks": [wl.i0, wl.i1], "keep": wl.keep,
+            "global_blocks": len(wl.global_blocks), "seed": a.seed,
+        },
+        "stages_ms": stage_ms,
+        "wall_ms_per_step": wall_ms,
+        "attention": {
+            "algorithmic_tflop": flops / 1e12,
+            "kernel_ms": stage_ms["block_sparse_attn"],
+            "tflops": attn_tflops,
+            "frac_of_mfma_peak": attn_tflops / peak,
+        },
+        "gather": {
+            "demanded_blocks": demanded,
+            "union_fraction": demanded / (wl.H * wl.n),
+            "algorithmic_bytes": gbytes,
+            "call_ms": stage_ms["demand_union_gather"],
+            "GBps": gbytes / (stage_ms["demand_union_gather"] * 1e-3) / 1e9,
+            "frac_of_hbm_peak": gbytes / (stage_ms["demand_union_gather"] * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+        },
+        "roofline": {
+            "bound": "mfma",
+            "achieved": attn_tflops,
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": attn_tflops / peak,
+            "traffic": traffic,
+            "traffic_note": traffic_note,
+        },
+        "cpu_baseline": None,
+    }
+    log(f"[bench] {wl.name}: {ms_per_step:.3f} ms/layer, attention {stage_ms['block_sparse_attn']:.3f} ms "
+        f"= {attn_tflops:.0f} TFLOP/s ({100 * attn_tflops / peak:.1f}% of peak), stages {stage_ms}")
+    if not a.no_cpu_baseline:
+        del Q, K, V, bufs, packed
+        torch.cuda.empty_cache()
+        log(f"[bench] timing the oracle on the host for ~{a.cpu_seconds:.0f}s")
+        rec["cpu_baseline"] = cpu_baseline(wl, q, k, v, a.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -115,43 +115,6 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 
     const int32_t* srow = sel + int64_t(wg) * keep;
     const int32_t* hslot = slot_of + int64_t(h) * n;
-    auto resolve = [&](int jj, int& slot, int& cnt) {
-        const int j = srow[jj];
-        slot = -1;
-        cnt = 0;
-        if (j >= 0 && j < n) {
-            const int s = hslot[j];
-            if (s >= 0 && s < capacity) {
-                slot = s;
-                cnt = min(BLK, L - j * BLK);
-            }
-        }
-    };
-
-    uint4 kreg[C::PER_THREAD], vreg[C::PER_THREAD];
-    auto fetch = [&](int slot) {
-        const uint4* ks = reinterpret_cast<const uint4*>(Kp + int64_t(slot) * BLK * D);
-        const uint4* vs = reinterpret_cast<const uint4*>(Vp + int64_t(slot) * BLK * D);
-#pragma unroll
-        for (int u = 0; u < C::PER_THREAD; ++u) {
-            kreg[u] = ks[u * C::THREADS + tid];
-            vreg[u] = vs[u * C::THREADS + tid];
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int u = 0; u < C::PER_THREAD; ++u) {
-            const int cid = u * C::THREADS + tid;
-            {
-                const int row = cid / (D / 8), ch = cid % (D / 8);
-                *reinterpret_cast<uint4*>(&lds_k[row * D + ((ch ^ swz<D>(row)) * 8)]) = kreg[u];
-            }
-            {
-                const int row = cid / (BLK / 8), ch = cid % (BLK / 8);
-                *reinterpret_cast<uint4*>(&lds_v[row * BLK + ((ch ^ swz<BLK>(row)) * 8)]) = vreg[u];
-            }
-        }
-    };
 
     floatx16 oacc[C::DT];
 #pragma unroll
@@ -159,35 +122,69 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     float m_run = -INFINITY;  // running max of scaled scores, log2 units
     float l_run = 0.f;        // this lane's partial row sum
 
-    int slot, cnt;
-    resolve(0, slot, cnt);
-    if (slot >= 0) fetch(slot);
+    // Slot and valid token count of kept entry jj; slot -1 marks an entry to skip.
+    int nxt_slot, nxt_cnt;
+    {
+        const int j = srow[0];
+        const int sl = (j >= 0 && j < n) ? hslot[j] : -1;
+        nxt_slot = (sl >= 0 && sl < capacity) ? sl : -1;
+        nxt_cnt = min(BLK, L - j * BLK);
+    }
+    // Prefetch registers. The load is unconditional (slot 0 always exists) so
+    // the buffers stay in VGPRs; skipped entries are simply not computed.
+    uint4 kreg[C::PER_THREAD], vreg[C::PER_THREAD];
+    {
+        const int64_t base = int64_t(nxt_slot < 0 ? 0 : nxt_slot) * BLK * D;
+        const uint4* ks = reinterpret_cast<const uint4*>(Kp + base);
+        const uint4* vs = reinterpret_cast<const uint4*>(Vp + base);
+#pragma unroll
+        for (int u = 0; u < C::PER_THREAD; ++u) {
+            kreg[u] = ks[u * C::THREADS + tid];
+            vreg[u] = vs[u * C::THREADS + tid];
+        }
+    }
 
     for (int jj = 0; jj < keep; ++jj) {
-        const int cur_slot = slot, cur_cnt = cnt;
+        const int cur_slot = nxt_slot, cur_cnt = nxt_cnt;
         __syncthreads();  // every wave is done reading the previous tile
-        if (cur_slot >= 0) stage();
+#pragma unroll
+        for (int u = 0; u < C::PER_THREAD; ++u) {
+            const int cid = u * C::THREADS + tid;
+            const int krow = cid / (D / 8), kch = cid % (D / 8);
+            *reinterpret_cast<uint4*>(&lds_k[krow * D + ((kch ^ swz<D>(krow)) * 8)]) = kreg[u];
+            const int vrow = cid / (BLK / 8), vch = cid % (BLK / 8);
+            *reinterpret_cast<uint4*>(&lds_v[vrow * BLK + ((vch ^ swz<BLK>(vrow)) * 8)]) = vreg[u];
+        }
         __syncthreads();
         if (jj + 1 < keep) {
-            resolve(jj + 1, slot, cnt);
-            if (slot >= 0) fetch(slot);
+            const int j = srow[jj + 1];
+            const int sl = (j >= 0 && j < n) ? hslot[j] : -1;
+            nxt_slot = (sl >= 0 && sl < capacity) ? sl : -1;
+            nxt_cnt = min(BLK, L - j * BLK);
+            const int64_t base = int64_t(nxt_slot < 0 ? 0 : nxt_slot) * BLK * D;
+            const uint4* ks = reinterpret_cast<const uint4*>(Kp + base);
+            const uint4* vs = reinterpret_cast<const uint4*>(Vp + base);
+#pragma unroll
+            for (int u = 0; u < C::PER_THREAD; ++u) {
+                kreg[u] = ks[u * C::THREADS + tid];
+                vreg[u] = vs[u * C::THREADS + tid];
+            }
         }
         if (cur_slot < 0) continue;
 
         // S^T tile: s[mt][rr] is key 32 mt + 16 (rr/8) + 8 g + rr%8 of query qi.
         floatx16 s[C::MT];
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt) {
-            floatx16 acc{};
-            const int krow = 32 * mt + sigma(qi);
-            const uint16_t* kr = lds_k + krow * D;
-            const int sw = swz<D>(krow);
+        for (int mt = 0; mt < C::MT; ++mt) s[mt] = floatx16{};
 #pragma unroll
-            for (int kt = 0; kt < C::KT; ++kt) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(kr + (((2 * kt + g) ^ sw) * 8));
-                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kt], acc, 0, 0, 0);
+        for (int kt = 0; kt < C::KT; ++kt) {
+#pragma unroll
+            for (int mt = 0; mt < C::MT; ++mt) {
+                const int krow = 32 * mt + sigma(qi);
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                    lds_k + krow * D + (((2 * kt + g) ^ swz<D>(krow)) * 8));
+                s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kt], s[mt], 0, 0, 0);
             }
-            s[mt] = acc;
         }
         if (cur_cnt < BLK) {
 #pragma unroll
@@ -203,7 +200,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 #pragma unroll
         for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
-            for (int rr = 0; rr < 16; ++rr) mx = fmaxf(mx, s[mt][rr]);
+            for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(mx, fmaxf(s[mt][rr], s[mt][rr + 1]));
         mx = pair_max(mx);
         const float m_new = fmaxf(m_run, mx * c2);
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);

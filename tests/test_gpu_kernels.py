@@ -196,8 +196,8 @@ def test_outputs_are_deterministic(gpu):
         out = sp.sparsp_demand_union_gather(g, m, Kd, Vd)
         O, lse = sp.sparsp_block_sparse_attn(g, Qd, sel, out["slot_of"], out["K_packed"],
                                              out["V_packed"], out_dtype=sp.BF16)
-        runs.append([x.cpu().numpy().tobytes() for x in (pq, pk, sc, m, sel, out["demand"],
-                                                       out["slot_of"], O, lse)])
+        outs = (pq, pk, sc, m, sel, out["demand"], out["slot_of"], O.view(P.torch().int16), lse)
+        runs.append([x.cpu().numpy().tobytes() for x in outs])
     assert runs[0] == runs[1]
 
 
