@@ -2,21 +2,32 @@
 // the packed K/V buffers (Eq. 1 over the kept blocks; softmax renormalised
 // over the kept keys, computed online in float32).
 //
-// Work split: one workgroup per (head, local query block), BLK/32 waves, each
-// wave owning 32 query rows. Workgroup ids are remapped so that each of the
-// eight XCDs walks a contiguous range of (head, query block): neighbouring
-// query blocks select overlapping KV blocks, which then hit in that XCD's L2.
+// Work split. One workgroup per (head, local query block) with 2*BLK/32
+// waves: wave w owns query group w % (BLK/32) (32 queries) and key half
+// w / (BLK/32) of every kept block (BLK/2 keys). Each wave runs its own online
+// softmax over its key halves (running max, running sum, output accumulator)
+// and the two halves of a query group are merged once at the end through
+// their log-sum-exp, so waves never wait on each other inside a tile. Splitting
+// keys instead of queries halves the LDS bytes each wave reads per tile and
+// keeps two waves per SIMD (256 VGPRs each) to overlap one wave's MFMAs with
+// the other's softmax.
 //
-// Per kept KV block the K tile ([BLK, D]) and the transposed V tile ([D, BLK])
-// are staged in LDS with an XOR swizzle of 16-byte chunks, so the MFMA operand
-// reads below are bank-conflict free. The next block's tiles are fetched into
-// registers while the current block is being computed.
+// Data movement. The kept blocks' K tile ([BLK, D]) and transposed V tile
+// ([D, BLK]) are copied HBM -> LDS with direct-to-LDS loads
+// (global_load_lds_dwordx4), double-buffered: the copy of block jj+1 is
+// issued right after the barrier that opens block jj and has the whole of
+// block jj's compute to land. One barrier per block. LDS rows carry an XOR
+// swizzle of their 16-byte chunks (applied through the source addresses of the
+// copies) so the MFMA operand reads are bank-conflict free. Workgroup ids are
+// remapped so that each of the eight XCDs walks a contiguous range of (head,
+// query block): neighbouring query blocks select overlapping KV blocks, which
+// then hit in that XCD's L2.
 //
 // Products use v_mfma_f32_32x32x16_bf16 with the score tile computed
 // transposed, S^T = K Q^T (A = K from LDS, B = Q^T from registers):
-//   * each lane then holds one query column (q = lane % 32) and 16 keys per
-//     32x32 tile, so the softmax row max and row sum are in-lane except for one
-//     exchange between lanes l and l^32;
+//   * each lane holds one query column (q = lane % 32) and 16 keys per 32x32
+//     tile, so the row max and row sum are in-lane except for one exchange
+//     between lanes l and l^32;
 //   * the output is accumulated transposed too, O^T = V^T P^T (A = V^T from
 //     the transposed V tile, B = P^T): the B operand is exactly the lane's own
 //     probabilities converted to bf16, no shuffles. For that to line up, the
@@ -26,6 +37,11 @@
 // MFMA operand layout (32x32x16, wave64): A lane l holds row l%32, k values
 // 8*(l/32) .. +7; B lane l holds column l%32, same k values; the 16 results
 // of lane l are column l%32, rows 8*(r/4) + 4*(l/32) + r%4.
+//
+// The running max is refreshed lazily: it only moves (and the accumulator is
+// rescaled) when some lane's block max exceeds it by more than 2^8, so most
+// blocks skip the rescale; probabilities then stay below 2^8, well inside
+// float32 and bf16 range, and the final normalisation uses the same max.
 #include "sparsp_internal.h"
 
 namespace sparsp {
@@ -37,6 +53,7 @@ typedef float floatx8 __attribute__((ext_vector_type(8)));
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kRescaleThreshold = 8.0f;  // log2 units
 
 __device__ __forceinline__ int sigma(int m) {  // swap bits 2 and 3
     return (m & ~0xC) | ((m & 4) << 1) | ((m & 8) >> 1);
@@ -46,7 +63,7 @@ __device__ __forceinline__ int sigma(int m) {  // swap bits 2 and 3
 // wide: the 16 rows read together by one quarter-wave land on distinct banks.
 template <int COLS>
 __device__ __forceinline__ int swz(int row) {
-    constexpr int NCH = COLS / 8;                       // chunks per row
+    constexpr int NCH = COLS / 8;                          // chunks per row
     constexpr int RP = (128 / COLS) > 1 ? 128 / COLS : 1;  // rows per 256 bytes
     return (row / RP) & (NCH - 1);
 }
@@ -65,31 +82,54 @@ __device__ __forceinline__ float pair_sum(float x) {
 
 template <int D, int BLK>
 struct Cfg {
-    static constexpr int NW = BLK / 32;           // waves
+    static constexpr int NQG = BLK / 32;          // query groups of 32
+    static constexpr int NW = 2 * NQG;            // waves: query group x key half
     static constexpr int THREADS = 64 * NW;
-    static constexpr int K_CHUNKS = BLK * D / 8;  // 16-byte chunks per tile
-    static constexpr int PER_THREAD = K_CHUNKS / THREADS;
-    static constexpr int MT = BLK / 32;           // key tiles of the score product
+    static constexpr int HALF = BLK / 2;          // keys per wave per block
+    static constexpr int MTW = HALF / 32;         // 32-key tiles per wave
     static constexpr int KT = D / 16;             // k steps of the score product
     static constexpr int DT = D / 32;             // d tiles of the output product
-    static constexpr int PT = BLK / 16;           // k steps of the output product
-    static_assert(K_CHUNKS % THREADS == 0, "tile must split evenly");
+    static constexpr int PTW = HALF / 16;         // k steps of the output product
+    static constexpr int TILE = BLK * D;          // elements per K (or V) tile
+    static constexpr int CHUNKS = TILE / 8;       // 16-byte chunks per tile
+    static constexpr int DMA = CHUNKS / THREADS;  // copies per lane per tile
+    static_assert(CHUNKS % THREADS == 0, "tile must split evenly");
+    static_assert(4 * TILE * 2 >= NQG * 64 * (DT * 16 + 2) * 4, "merge area must fit");
 };
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Issue the direct-to-LDS copies of one tile. LDS chunk position p (row p/NCH,
+// physical chunk p%NCH) receives logical chunk (p%NCH) ^ swz(row) of that row.
+template <int COLS, int NW, int DMA>
+__device__ __forceinline__ void copy_tile(const uint16_t* __restrict__ src, uint16_t* dst, int wave,
+                                          int lane) {
+    constexpr int NCH = COLS / 8;
+#pragma unroll
+    for (int u = 0; u < DMA; ++u) {
+        const int base = (u * NW + wave) * 64;  // first chunk this wave writes
+        const int p = base + lane;
+        const int row = p / NCH, pc = p % NCH;
+        const uint16_t* g = src + row * COLS + ((pc ^ swz<COLS>(row)) * 8);
+        __builtin_amdgcn_global_load_lds(g, (lds_void*)(dst + base * 8), 16, 0, 0);
+    }
+}
+
 template <int D, int BLK, bool OUT_BF16>
-__global__ __launch_bounds__(2 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(4 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict__ sel,
                       const int32_t* __restrict__ slot_of, const uint16_t* __restrict__ Kp,
                       const uint16_t* __restrict__ Vp, void* __restrict__ O,
                       float* __restrict__ lse, int H, int L, int n, int i0, int nq, int keep,
                       int64_t capacity, float c2 /* scale * log2(e) */, int remap) {
     using C = Cfg<D, BLK>;
-    __shared__ __attribute__((aligned(16))) uint16_t lds_k[BLK * D];
-    __shared__ __attribute__((aligned(16))) uint16_t lds_v[D * BLK];
+    // [buffer][K tile | V tile]; reused for the final merge.
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][C::TILE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int qi = lane & 31, g = lane >> 5;
+    const int qg = wave % C::NQG, kh = wave / C::NQG;
 
     // Workgroup -> (head, local query block), XCD-contiguous when remap is on.
     const int G = H * nq;
@@ -99,8 +139,27 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         wg = xcd * per + min(xcd, rem) + idx;
     }
     const int h = wg / nq, r = wg % nq;
-    const int qtok = (i0 + r) * BLK + wave * 32 + qi;
+    const int qtok = (i0 + r) * BLK + qg * 32 + qi;
     const bool qvalid = qtok < L;
+
+    const int32_t* srow = sel + int64_t(wg) * keep;
+    const int32_t* hslot = slot_of + int64_t(h) * n;
+
+    // Slot of kept entry jj, or -1 to skip it; the copy then reads slot 0
+    // (always present) and the block is not computed.
+    auto slot_at = [&](int jj) {
+        const int j = srow[jj];
+        const int sl = (j >= 0 && j < n) ? hslot[j] : -1;
+        return (sl >= 0 && sl < capacity) ? sl : -1;
+    };
+    auto issue = [&](int jj, int buf) {
+        const int sl = slot_at(jj);
+        const int64_t off = int64_t(sl < 0 ? 0 : sl) * C::TILE;
+        copy_tile<D, C::NW, C::DMA>(Kp + off, &lds[buf][0][0], wave, lane);
+        copy_tile<BLK, C::NW, C::DMA>(Vp + off, &lds[buf][1][0], wave, lane);
+    };
+
+    issue(0, 0);
 
     // Q^T operand: lane holds Q[qtok][16 kt + 8 g .. +7] for every k step.
     bf16x8 qf[C::KT];
@@ -113,126 +172,115 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         }
     }
 
-    const int32_t* srow = sel + int64_t(wg) * keep;
-    const int32_t* hslot = slot_of + int64_t(h) * n;
-
     floatx16 oacc[C::DT];
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = floatx16{};
-    float m_run = -INFINITY;  // running max of scaled scores, log2 units
+    float m_run = -INFINITY;  // running (lazy) max of scaled scores, log2 units
     float l_run = 0.f;        // this lane's partial row sum
 
-    // Slot and valid token count of kept entry jj; slot -1 marks an entry to skip.
-    int nxt_slot, nxt_cnt;
-    {
-        const int j = srow[0];
-        const int sl = (j >= 0 && j < n) ? hslot[j] : -1;
-        nxt_slot = (sl >= 0 && sl < capacity) ? sl : -1;
-        nxt_cnt = min(BLK, L - j * BLK);
-    }
-    // Prefetch registers. The load is unconditional (slot 0 always exists) so
-    // the buffers stay in VGPRs; skipped entries are simply not computed.
-    uint4 kreg[C::PER_THREAD], vreg[C::PER_THREAD];
-    {
-        const int64_t base = int64_t(nxt_slot < 0 ? 0 : nxt_slot) * BLK * D;
-        const uint4* ks = reinterpret_cast<const uint4*>(Kp + base);
-        const uint4* vs = reinterpret_cast<const uint4*>(Vp + base);
-#pragma unroll
-        for (int u = 0; u < C::PER_THREAD; ++u) {
-            kreg[u] = ks[u * C::THREADS + tid];
-            vreg[u] = vs[u * C::THREADS + tid];
-        }
-    }
-
     for (int jj = 0; jj < keep; ++jj) {
-        const int cur_slot = nxt_slot, cur_cnt = nxt_cnt;
-        __syncthreads();  // every wave is done reading the previous tile
-#pragma unroll
-        for (int u = 0; u < C::PER_THREAD; ++u) {
-            const int cid = u * C::THREADS + tid;
-            const int krow = cid / (D / 8), kch = cid % (D / 8);
-            *reinterpret_cast<uint4*>(&lds_k[krow * D + ((kch ^ swz<D>(krow)) * 8)]) = kreg[u];
-            const int vrow = cid / (BLK / 8), vch = cid % (BLK / 8);
-            *reinterpret_cast<uint4*>(&lds_v[vrow * BLK + ((vch ^ swz<BLK>(vrow)) * 8)]) = vreg[u];
-        }
-        __syncthreads();
-        if (jj + 1 < keep) {
-            const int j = srow[jj + 1];
-            const int sl = (j >= 0 && j < n) ? hslot[j] : -1;
-            nxt_slot = (sl >= 0 && sl < capacity) ? sl : -1;
-            nxt_cnt = min(BLK, L - j * BLK);
-            const int64_t base = int64_t(nxt_slot < 0 ? 0 : nxt_slot) * BLK * D;
-            const uint4* ks = reinterpret_cast<const uint4*>(Kp + base);
-            const uint4* vs = reinterpret_cast<const uint4*>(Vp + base);
-#pragma unroll
-            for (int u = 0; u < C::PER_THREAD; ++u) {
-                kreg[u] = ks[u * C::THREADS + tid];
-                vreg[u] = vs[u * C::THREADS + tid];
-            }
-        }
+        const int buf = jj & 1;
+        const int j = srow[jj];
+        const int cur_slot = slot_at(jj);
+        const int cur_cnt = min(BLK, L - j * BLK);
+        __syncthreads();  // copies of block jj landed; everyone is done with block jj-1
+        if (jj + 1 < keep) issue(jj + 1, buf ^ 1);
         if (cur_slot < 0) continue;
 
-        // S^T tile: s[mt][rr] is key 32 mt + 16 (rr/8) + 8 g + rr%8 of query qi.
-        floatx16 s[C::MT];
+        const uint16_t* lk = &lds[buf][0][0];
+        const uint16_t* lv = &lds[buf][1][0];
+
+        // S^T for this wave's key half: s[mt][rr] is key
+        // HALF*kh + 32 mt + 16 (rr/8) + 8 g + rr%8 of query qi.
+        floatx16 s[C::MTW];
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt) s[mt] = floatx16{};
+        for (int mt = 0; mt < C::MTW; ++mt) s[mt] = floatx16{};
 #pragma unroll
         for (int kt = 0; kt < C::KT; ++kt) {
 #pragma unroll
-            for (int mt = 0; mt < C::MT; ++mt) {
-                const int krow = 32 * mt + sigma(qi);
+            for (int mt = 0; mt < C::MTW; ++mt) {
+                const int krow = C::HALF * kh + 32 * mt + sigma(qi);
                 const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                    lds_k + krow * D + (((2 * kt + g) ^ swz<D>(krow)) * 8));
+                    lk + krow * D + (((2 * kt + g) ^ swz<D>(krow)) * 8));
                 s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kt], s[mt], 0, 0, 0);
             }
         }
         if (cur_cnt < BLK) {
 #pragma unroll
-            for (int mt = 0; mt < C::MT; ++mt)
+            for (int mt = 0; mt < C::MTW; ++mt)
 #pragma unroll
                 for (int rr = 0; rr < 16; ++rr) {
-                    const int key = 32 * mt + 16 * (rr >> 3) + 8 * g + (rr & 7);
+                    const int key = C::HALF * kh + 32 * mt + 16 * (rr >> 3) + 8 * g + (rr & 7);
                     if (key >= cur_cnt) s[mt][rr] = -INFINITY;
                 }
         }
 
         float mx = -INFINITY;
 #pragma unroll
-        for (int mt = 0; mt < C::MT; ++mt)
+        for (int mt = 0; mt < C::MTW; ++mt)
 #pragma unroll
             for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(mx, fmaxf(s[mt][rr], s[mt][rr + 1]));
-        mx = pair_max(mx);
-        const float m_new = fmaxf(m_run, mx * c2);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        m_run = m_new;
-        l_run *= alpha;
+        mx = pair_max(mx) * c2;
+        // Lazy max: move it only when some lane's block max exceeds it by more
+        // than the threshold (always on the first block a lane sees).
+        if (__ballot(mx > m_run + kRescaleThreshold)) {
+            const float m_new = fmaxf(m_run, mx);
+            const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            l_run *= alpha;
 #pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
+            for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
+        }
+        const float m_use = (m_run == -INFINITY) ? 0.0f : m_run;
 
 #pragma unroll
-        for (int t = 0; t < C::PT; ++t) {
+        for (int t = 0; t < C::PTW; ++t) {
             const int mt = t >> 1, hf = t & 1;
             floatx8 p;
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
-                p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, -m_new));
+                p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, -m_use));
                 l_run += p[v];
             }
             const bf16x8 pb = __builtin_convertvector(p, bf16x8);
+            const int tg = C::PTW * kh + t;  // 16-key step within the block
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt) {
                 const int vrow = 32 * dt + qi;
                 const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                    lds_v + vrow * BLK + (((2 * t + g) ^ swz<BLK>(vrow)) * 8));
+                    lv + vrow * BLK + (((2 * tg + g) ^ swz<BLK>(vrow)) * 8));
                 oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
             }
         }
     }
 
-    const float l_tot = pair_sum(l_run);
+    // Merge the two key halves of each query group through their log-sum-exp.
+    const float l_half = pair_sum(l_run);
+    __syncthreads();  // every wave is done with the tiles
+    float* mrg = reinterpret_cast<float*>(&lds[0][0][0]);
+    constexpr int REGS = C::DT * 16;
+    float* mine = mrg + qg * 64 * (REGS + 2);
+    if (kh == 1) {
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+            for (int rr = 0; rr < 16; ++rr) mine[(dt * 16 + rr) * 64 + lane] = oacc[dt][rr];
+        mine[REGS * 64 + lane] = m_run;
+        mine[(REGS + 1) * 64 + lane] = l_half;
+    }
+    __syncthreads();
+    if (kh == 1) return;
+
+    const float m_b = mine[REGS * 64 + lane];
+    const float l_b = mine[(REGS + 1) * 64 + lane];
+    const float m = fmaxf(m_run, m_b);
+    const float w_a = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m);
+    const float w_b = (m_b == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_b - m);
+    const float l_tot = l_half * w_a + l_b * w_b;
     const bool live = qvalid && l_tot > 0.f;
     const float inv = live ? 1.0f / l_tot : 0.f;
-    const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + wave * 32 + qi;
+    const float fa = w_a * inv, fb = w_b * inv;
+    const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + qg * 32 + qi;
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt) {
 #pragma unroll
@@ -240,7 +288,10 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             const int d0 = 32 * dt + 8 * q4 + 4 * g;
             float o4[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) o4[u] = oacc[dt][4 * q4 + u] * inv;
+            for (int u = 0; u < 4; ++u) {
+                const int rr = 4 * q4 + u;
+                o4[u] = live ? oacc[dt][rr] * fa + mine[(dt * 16 + rr) * 64 + lane] * fb : 0.f;
+            }
             if constexpr (OUT_BF16) {
                 uint16_t* op = static_cast<uint16_t*>(O) + orow * D + d0;
                 uint2 w;
@@ -253,7 +304,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             }
         }
     }
-    if (lse && g == 0) lse[orow] = live ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (lse && g == 0) lse[orow] = live ? (m + __log2f(l_tot)) * kLn2 : -INFINITY;
 }
 
 template <int D, int BLK>
