@@ -48,6 +48,8 @@ def parse_args(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="wall-clock budget of the oracle sample")
+    ap.add_argument("--cache-dir", default=None,
+                    help="keep generated inputs as .npy files here and reuse them")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of this many MiB (for counter calibration)")
     return ap.parse_args(argv)
@@ -66,6 +68,21 @@ def copy_calibration(mib: int):
         dst.copy_(src)
     torch.cuda.synchronize()
     log(f"copied {mib} MiB x 5")
+
+
+def load_inputs(wl, seed, cache_dir, make_qkv):
+    """Generate the workload's inputs, or reuse a copy saved by an earlier run."""
+    import numpy as np
+    if cache_dir:
+        paths = [os.path.join(cache_dir, f"{wl.config_id}_{seed}_{t}.npy") for t in "qkv"]
+        if all(os.path.exists(p) for p in paths):
+            return tuple(np.load(p) for p in paths)
+    q, k, v = make_qkv(wl, seed=seed)
+    if cache_dir:
+        os.makedirs(cache_dir, exist_ok=True)
+        for p, x in zip(paths, (q, k, v)):
+            np.save(p, x)
+    return q, k, v
 
 
 def file_sha(path):
@@ -167,8 +184,8 @@ def main(argv=None) -> int:
 
     wl = get_workload(a.workload)
     t0 = time.time()
-    q, k, v = make_qkv(wl, seed=a.seed)
-    log(f"[bench] generated {wl.name} inputs in {time.time() - t0:.1f}s")
+    q, k, v = load_inputs(wl, a.seed, a.cache_dir, make_qkv)
+    log(f"[bench] {wl.name} inputs ready in {time.time() - t0:.1f}s")
 
     def dev(x):
         if wl.dtype == "bf16":

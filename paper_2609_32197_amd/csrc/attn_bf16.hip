@@ -99,20 +99,32 @@ struct Cfg {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Issue the direct-to-LDS copies of one tile. LDS chunk position p (row p/NCH,
-// physical chunk p%NCH) receives logical chunk (p%NCH) ^ swz(row) of that row.
-template <int COLS, int NW, int DMA>
-__device__ __forceinline__ void copy_tile(const uint16_t* __restrict__ src, uint16_t* dst, int wave,
-                                          int lane) {
+// Byte offset, within a packed tile of rows COLS bf16 wide, of the 16-byte
+// chunk that lands at LDS chunk position p: LDS row p/NCH, physical chunk
+// p%NCH holds logical chunk (p%NCH) ^ swz(row). Constant for the whole
+// kernel, so each lane computes its copy offsets once.
+template <int COLS>
+__device__ __forceinline__ int chunk_src_offset(int p) {
     constexpr int NCH = COLS / 8;
+    const int row = p / NCH, pc = p % NCH;
+    return (row * COLS + ((pc ^ swz<COLS>(row)) * 8)) * 2;
+}
+
+// Direct-to-LDS copy of one tile through a buffer resource rooted at the
+// tile: per copy one SGPR base (the LDS destination) and one precomputed VGPR
+// offset. Reads outside the tile return zero instead of faulting.
+template <int NW, int DMA>
+__device__ __forceinline__ void copy_tile(const uint16_t* tile, int tile_bytes, uint16_t* dst,
+                                          const int (&voff)[DMA], int wave) {
+#if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist only in the device pass
+    __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)tile, (short)0, tile_bytes, 0x00020000);
 #pragma unroll
     for (int u = 0; u < DMA; ++u) {
-        const int base = (u * NW + wave) * 64;  // first chunk this wave writes
-        const int p = base + lane;
-        const int row = p / NCH, pc = p % NCH;
-        const uint16_t* g = src + row * COLS + ((pc ^ swz<COLS>(row)) * 8);
-        __builtin_amdgcn_global_load_lds(g, (lds_void*)(dst + base * 8), 16, 0, 0);
+        uint16_t* d = dst + (u * NW + wave) * 64 * 8;  // this wave's 1 KB of the tile
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)d, 16, voff[u], 0, 0, 0);
     }
+#endif
 }
 
 template <int D, int BLK, bool OUT_BF16>
@@ -125,6 +137,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     using C = Cfg<D, BLK>;
     // [buffer][K tile | V tile]; reused for the final merge.
     __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][C::TILE];
+    // Per kept entry: 2 * slot + (block is the partial last one), or -1 to skip.
+    extern __shared__ int32_t codes[];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -142,24 +156,35 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     const int qtok = (i0 + r) * BLK + qg * 32 + qi;
     const bool qvalid = qtok < L;
 
-    const int32_t* srow = sel + int64_t(wg) * keep;
-    const int32_t* hslot = slot_of + int64_t(h) * n;
+    // Resolve the kept list once: sel -> slot (and partial-block flag).
+    {
+        const int32_t* srow = sel + int64_t(wg) * keep;
+        const int32_t* hslot = slot_of + int64_t(h) * n;
+        const bool ragged = (L % BLK) != 0;
+        for (int jj = tid; jj < keep; jj += C::THREADS) {
+            const int j = srow[jj];
+            int code = -1;
+            if (j >= 0 && j < n) {
+                const int sl = hslot[j];
+                if (sl >= 0 && sl < capacity && sl < (1 << 30))
+                    code = 2 * sl + ((ragged && j == n - 1) ? 1 : 0);
+            }
+            codes[jj] = code;
+        }
+    }
 
-    // Slot of kept entry jj, or -1 to skip it; the copy then reads slot 0
-    // (always present) and the block is not computed.
-    auto slot_at = [&](int jj) {
-        const int j = srow[jj];
-        const int sl = (j >= 0 && j < n) ? hslot[j] : -1;
-        return (sl >= 0 && sl < capacity) ? sl : -1;
+    int kvoff[C::DMA], vvoff[C::DMA];
+#pragma unroll
+    for (int u = 0; u < C::DMA; ++u) {
+        const int p = (u * C::NW + wave) * 64 + lane;
+        kvoff[u] = chunk_src_offset<D>(p);
+        vvoff[u] = chunk_src_offset<BLK>(p);
+    }
+    auto issue = [&](int code, int buf) {
+        const int64_t off = int64_t(code < 0 ? 0 : (code >> 1)) * C::TILE;
+        copy_tile<C::NW, C::DMA>(Kp + off, C::TILE * 2, &lds[buf][0][0], kvoff, wave);
+        copy_tile<C::NW, C::DMA>(Vp + off, C::TILE * 2, &lds[buf][1][0], vvoff, wave);
     };
-    auto issue = [&](int jj, int buf) {
-        const int sl = slot_at(jj);
-        const int64_t off = int64_t(sl < 0 ? 0 : sl) * C::TILE;
-        copy_tile<D, C::NW, C::DMA>(Kp + off, &lds[buf][0][0], wave, lane);
-        copy_tile<BLK, C::NW, C::DMA>(Vp + off, &lds[buf][1][0], wave, lane);
-    };
-
-    issue(0, 0);
 
     // Q^T operand: lane holds Q[qtok][16 kt + 8 g .. +7] for every k step.
     bf16x8 qf[C::KT];
@@ -171,21 +196,28 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             qf[kt] = __builtin_bit_cast(bf16x8, v);
         }
     }
+    __syncthreads();  // codes visible
+    int code = codes[0];
+    issue(code, 0);
+    int next_code = keep > 1 ? codes[1] : -1;
 
     floatx16 oacc[C::DT];
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = floatx16{};
     float m_run = -INFINITY;  // running (lazy) max of scaled scores, log2 units
     float l_run = 0.f;        // this lane's partial row sum
+    const int last_cnt = L - (L / BLK) * BLK;  // valid keys of a partial last block
 
     for (int jj = 0; jj < keep; ++jj) {
         const int buf = jj & 1;
-        const int j = srow[jj];
-        const int cur_slot = slot_at(jj);
-        const int cur_cnt = min(BLK, L - j * BLK);
+        const int cur = code;
         __syncthreads();  // copies of block jj landed; everyone is done with block jj-1
-        if (jj + 1 < keep) issue(jj + 1, buf ^ 1);
-        if (cur_slot < 0) continue;
+        if (jj + 1 < keep) {
+            issue(next_code, buf ^ 1);
+            code = next_code;
+            next_code = (jj + 2 < keep) ? codes[jj + 2] : -1;
+        }
+        if (cur < 0) continue;
 
         const uint16_t* lk = &lds[buf][0][0];
         const uint16_t* lv = &lds[buf][1][0];
@@ -205,13 +237,13 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kt], s[mt], 0, 0, 0);
             }
         }
-        if (cur_cnt < BLK) {
+        if (cur & 1) {  // partial last block: keys past L do not exist
 #pragma unroll
             for (int mt = 0; mt < C::MTW; ++mt)
 #pragma unroll
                 for (int rr = 0; rr < 16; ++rr) {
                     const int key = C::HALF * kh + 32 * mt + 16 * (rr >> 3) + 8 * g + (rr & 7);
-                    if (key >= cur_cnt) s[mt][rr] = -INFINITY;
+                    if (key >= last_cnt) s[mt][rr] = -INFINITY;
                 }
         }
 
@@ -219,7 +251,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 #pragma unroll
         for (int mt = 0; mt < C::MTW; ++mt)
 #pragma unroll
-            for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(mx, fmaxf(s[mt][rr], s[mt][rr + 1]));
+            for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(fmaxf(mx, s[mt][rr]), s[mt][rr + 1]);
         mx = pair_max(mx) * c2;
         // Lazy max: move it only when some lane's block max exceeds it by more
         // than the threshold (always on the first block a lane sees).
@@ -233,6 +265,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         }
         const float m_use = (m_run == -INFINITY) ? 0.0f : m_run;
 
+        float lsum[2] = {0.f, 0.f};
 #pragma unroll
         for (int t = 0; t < C::PTW; ++t) {
             const int mt = t >> 1, hf = t & 1;
@@ -240,7 +273,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
                 p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, -m_use));
-                l_run += p[v];
+                lsum[v & 1] += p[v];
             }
             const bf16x8 pb = __builtin_convertvector(p, bf16x8);
             const int tg = C::PTW * kh + t;  // 16-key step within the block
@@ -252,6 +285,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
             }
         }
+        l_run += lsum[0] + lsum[1];
     }
 
     // Merge the two key halves of each query group through their log-sum-exp.
@@ -315,12 +349,13 @@ hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int ke
     const int G = g.H * g.nq;
     const float c2 = scale * kLog2e;
     const int remap = 1;
+    const size_t dyn = size_t(keep) * sizeof(int32_t);
     if (out_bf16)
-        attn_bf16_kernel<D, BLK, true><<<G, C::THREADS, 0, s>>>(
+        attn_bf16_kernel<D, BLK, true><<<G, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.H, g.L, g.n, g.i0, g.nq, keep, cap, c2, remap);
     else
-        attn_bf16_kernel<D, BLK, false><<<G, C::THREADS, 0, s>>>(
+        attn_bf16_kernel<D, BLK, false><<<G, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.H, g.L, g.n, g.i0, g.nq, keep, cap, c2, remap);
     return hipGetLastError();
