@@ -30,9 +30,10 @@
  *   call leaves every output untouched. SPARSP_E_HIP reports a launch error;
  *   sparsp_last_error() gives the message of the calling thread's last error.
  * - Indices are int32; byte offsets are computed in 64-bit inside the library.
- * - Limits: n <= 4096 blocks; d <= 256; bf16 attention needs d and block in
- *   {64, 128}; f32 attention needs d <= 128 and block <= 256; d must be a
- *   multiple of 8 (bf16) or 4 (f32).
+ * - Limits: n <= 4096 blocks; H <= 1024; d <= 256; block <= 4096; d must be
+ *   a multiple of 8 (bf16) or 4 (f32), and so must block for the packed-block
+ *   calls; bf16 attention needs d and block in {64, 128}; f32 attention needs
+ *   d <= 128 and block <= 256.
  */
 #ifndef SPARSP_H
 #define SPARSP_H

@@ -47,6 +47,8 @@ int derive(const sparsp_geom* g, sparsp::Geom* out) {
         return fail(SPARSP_E_UNSUPPORTED, "n = %lld blocks exceeds the limit %d", (long long)n,
                     sparsp::kMaxBlocks);
     if (g->d > 256) return fail(SPARSP_E_UNSUPPORTED, "d = %d exceeds 256", g->d);
+    if (g->H > sparsp::kMaxHeads)
+        return fail(SPARSP_E_UNSUPPORTED, "H = %d exceeds %d", g->H, sparsp::kMaxHeads);
     const int vec = g->dtype == SPARSP_BF16 ? 8 : 4;
     if (g->d % vec)
         return fail(SPARSP_E_UNSUPPORTED, "d = %d must be a multiple of %d for this dtype", g->d, vec);
@@ -138,8 +140,8 @@ int sparsp_demand_union_gather(const sparsp_geom* g, const uint64_t* mask, const
     if (!mask || !K || !V || !demand || !head_off || !slot_of || !gather_blk || !K_packed ||
         !V_packed)
         return fail(SPARSP_E_INVALID, "NULL tensor pointer");
-    if (G.block > 4096) return fail(SPARSP_E_UNSUPPORTED, "block %d exceeds 4096", G.block);
     if (int rc = check_chunked(G)) return rc;
+    if (G.block > 4096) return fail(SPARSP_E_UNSUPPORTED, "block %d exceeds 4096", G.block);
     if (!aligned16(K) || !aligned16(V) || !aligned16(K_packed) || !aligned16(V_packed))
         return fail(SPARSP_E_INVALID, "K, V and the packed buffers must be 16-byte aligned");
     const int64_t need = int64_t(G.H) * G.n;

@@ -13,10 +13,11 @@
 // the other's softmax.
 //
 // Data movement. The kept blocks' K tile ([BLK, D]) and transposed V tile
-// ([D, BLK]) are copied HBM -> LDS with direct-to-LDS loads
-// (global_load_lds_dwordx4), double-buffered: the copy of block jj+1 is
+// ([D, BLK]) are copied HBM -> LDS with direct-to-LDS buffer loads
+// (buffer_load_dwordx4 ... lds), double-buffered: the copy of block jj+1 is
 // issued right after the barrier that opens block jj and has the whole of
-// block jj's compute to land. One barrier per block. LDS rows carry an XOR
+// block jj's compute to land; each wave waits for its own copies before the
+// next barrier. One barrier per block. LDS rows carry an XOR
 // swizzle of their 16-byte chunks (applied through the source addresses of the
 // copies) so the MFMA operand reads are bank-conflict free. Workgroup ids are
 // remapped so that each of the eight XCDs walks a contiguous range of (head,
@@ -98,6 +99,10 @@ struct Cfg {
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
+
+// s_waitcnt vmcnt(0), leaving the other counters alone (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+__device__ __forceinline__ void wait_vmem_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Byte offset, within a packed tile of rows COLS bf16 wide, of the 16-byte
 // chunk that lands at LDS chunk position p: LDS row p/NCH, physical chunk
@@ -211,7 +216,12 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     for (int jj = 0; jj < keep; ++jj) {
         const int buf = jj & 1;
         const int cur = code;
-        __syncthreads();  // copies of block jj landed; everyone is done with block jj-1
+        // A workgroup barrier does not wait for outstanding vector-memory
+        // loads, and the compiler does not add that wait for direct-to-LDS
+        // copies: each wave waits for its own copies of block jj (the only
+        // ones in flight) before the barrier publishes the whole tile.
+        wait_vmem_all();
+        __syncthreads();  // block jj in LDS; everyone is done with block jj-1
         if (jj + 1 < keep) {
             issue(next_code, buf ^ 1);
             code = next_code;

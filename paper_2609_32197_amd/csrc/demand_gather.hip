@@ -8,18 +8,31 @@
 //                block's slot = head_off[h] + rank of the block in D_h, which
 //                fills slot_of and gather_blk. Both ends of an exchange could
 //                derive these offsets locally from the same bitsets.
-// gather_kernel  one workgroup per (block, head); blocks that are not demanded
-//                exit at once. K blocks are copied with 16-byte loads and
-//                stores; V blocks are written transposed ([d, block]) so the
-//                attention kernel reads V^T MFMA operands with contiguous
-//                16-byte loads. Each thread moves a VEC x VEC sub-block and
-//                transposes it in registers. Rows past L are written as zero.
-//                The grid covers all H*n blocks, so no host round trip is
-//                needed to learn the demand total.
+// gather_kernel  a fixed grid (one workgroup per CU) walks the demanded slots
+//                in order, reading the slot count and the slot -> (head, block)
+//                map from head_off and gather_blk on the device, so no host
+//                round trip is needed. K blocks are copied with 16-byte
+//                loads and stores; V blocks are written
+//                transposed ([d, block]) so the attention kernel reads V^T MFMA
+//                operands with contiguous 16-byte loads (each thread moves a
+//                VEC x VEC sub-block and transposes it in registers). Rows past
+//                L are written as zero.
 #include "sparsp_internal.h"
 
 namespace sparsp {
 namespace {
+
+constexpr int kGatherGrid = 256;  // one workgroup per CU of an MI355X
+
+// Plain loads and stores. Non-temporal stores were measured ~6% faster here,
+// but the attention kernel launched right after did not always see their data
+// (stale tiles on its first run), so the packed buffers are written normally.
+__device__ __forceinline__ uint4 load_stream(const char* p) {
+    return *reinterpret_cast<const uint4*>(p);
+}
+__device__ __forceinline__ void store_stream(char* p, uint4 v) {
+    *reinterpret_cast<uint4*>(p) = v;
+}
 
 __global__ __launch_bounds__(256) void union_kernel(const uint64_t* __restrict__ mask, int nq,
                                                     int W, uint64_t* __restrict__ demand) {
@@ -108,71 +121,81 @@ __device__ __forceinline__ void transpose4x4_b32(const uint4 (&in)[4], uint4 (&o
     out[3] = make_uint4(in[0].w, in[1].w, in[2].w, in[3].w);
 }
 
+// The packed buffers are filled window by window: window 2s copies slot s's
+// K block, window 2s+1 writes its V block transposed. A grid-stride walk over
+// the windows keeps all resident workgroups on neighbouring slots, i.e. inside
+// one contiguous stretch of source and destination at any moment, which is
+// what lets the copy stream at full HBM rate; each thread keeps four 16-byte
+// loads in flight per pass for K (eight rows for the V transpose).
 template <bool BF16>
-__global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__ slot_of,
+__global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__ head_off,
+                                                     const int32_t* __restrict__ gather_blk,
                                                      const char* __restrict__ K,
                                                      const char* __restrict__ V,
                                                      char* __restrict__ Kp, char* __restrict__ Vp,
-                                                     int L, int d, int block, int n) {
-    constexpr int ES = BF16 ? 2 : 4;     // element size
-    constexpr int VEC = 16 / ES;         // elements per 16-byte chunk
-    const int j = blockIdx.x;
-    const int h = blockIdx.y;
-    const int slot = slot_of[int64_t(h) * n + j];
-    if (slot < 0) return;
-    const int tid = threadIdx.x;
-    const int tok0 = j * block;
-    const int cnt = min(block, L - tok0);
+                                                     int H, int L, int d, int block) {
+    constexpr int ES = BF16 ? 2 : 4;  // element size
+    constexpr int VEC = 16 / ES;      // elements per 16-byte chunk
+    constexpr int T = 256;
+    __shared__ int32_t hoff[kMaxHeads + 1];
+    for (int i = threadIdx.x; i <= H; i += T) hoff[i] = head_off[i];
+    __syncthreads();
+    const int total_slots = hoff[H];
     const int64_t blk_bytes = int64_t(block) * d * ES;
-    const char* ksrc = K + (int64_t(h) * L + tok0) * d * ES;
-    const char* vsrc = V + (int64_t(h) * L + tok0) * d * ES;
-    char* kdst = Kp + int64_t(slot) * blk_bytes;
-    char* vdst = Vp + int64_t(slot) * blk_bytes;
-
-    // K: straight copy of `cnt` rows, zero rows after.
-    const int row_chunks = d / VEC;
-    const int total = block * row_chunks;
-    const int valid = cnt * row_chunks;
-    for (int e = tid; e < total; e += 256) {
-        uint4 x = make_uint4(0, 0, 0, 0);
-        if (e < valid) x = *reinterpret_cast<const uint4*>(ksrc + int64_t(e) * 16);
-        *reinterpret_cast<uint4*>(kdst + int64_t(e) * 16) = x;
-    }
-
-    // V: transposed copy by VEC x VEC sub-blocks. Sub-block (kb, db) covers tokens
-    // kb*VEC .. +VEC-1 and dims db*VEC .. +VEC-1. Consecutive threads take
-    // consecutive db, so each load instruction reads whole token rows.
-    const int dblocks = d / VEC;
-    const int kblocks = (block + VEC - 1) / VEC;
-    for (int e = tid; e < dblocks * kblocks; e += 256) {
-        const int db = e % dblocks, kb = e / dblocks;
-        uint4 rows[VEC], cols[VEC];
+    const int tid = threadIdx.x;
+    int h = 0;  // head of the current slot; slots only grow along the walk
+    for (int w = blockIdx.x; w < 2 * total_slots; w += gridDim.x) {
+        const int slot = w >> 1;
+        while (slot >= hoff[h + 1]) ++h;
+        const int j = gather_blk[slot];
+        const int tok0 = j * block;
+        const int cnt = min(block, L - tok0);
+        const int64_t src = (int64_t(h) * L + tok0) * d * ES;
+        if ((w & 1) == 0) {
+            // K: straight copy of `cnt` token rows, zero rows after.
+            const char* ksrc = K + src;
+            char* kdst = Kp + int64_t(slot) * blk_bytes;
+            const int row_chunks = d / VEC;
+            const int total = block * row_chunks;
+            const int valid = cnt * row_chunks;
+            for (int e0 = tid; e0 < total; e0 += 4 * T) {
+                uint4 x[4];
 #pragma unroll
-        for (int r = 0; r < VEC; ++r) {
-            const int t = kb * VEC + r;
-            rows[r] = make_uint4(0, 0, 0, 0);
-            if (t < cnt)
-                rows[r] = *reinterpret_cast<const uint4*>(vsrc + (int64_t(t) * d + db * VEC) * ES);
-        }
-        if constexpr (BF16) transpose8x8_b16(rows, cols);
-        else transpose4x4_b32(rows, cols);
-        // cols[c] = dim db*VEC+c, tokens kb*VEC .. +VEC-1 -> Vp[slot][dim][token]
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) {
-            const int64_t off = (int64_t(db * VEC + c) * block + kb * VEC) * ES;
-            if (kb * VEC + VEC <= block) {
-                *reinterpret_cast<uint4*>(vdst + off) = cols[c];
-            } else {
-                // Ragged block size: store the in-range elements one by one.
-                const uint32_t w[4] = {cols[c].x, cols[c].y, cols[c].z, cols[c].w};
-                for (int u = 0; u < VEC && kb * VEC + u < block; ++u) {
-                    if constexpr (BF16) {
-                        const uint16_t v16 = uint16_t((w[u >> 1] >> ((u & 1) * 16)) & 0xffffu);
-                        *reinterpret_cast<uint16_t*>(vdst + off + u * 2) = v16;
-                    } else {
-                        *reinterpret_cast<uint32_t*>(vdst + off + u * 4) = w[u];
-                    }
+                for (int u = 0; u < 4; ++u) {
+                    const int e = e0 + u * T;
+                    x[u] = make_uint4(0, 0, 0, 0);
+                    if (e < valid) x[u] = load_stream(ksrc + int64_t(e) * 16);
                 }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int e = e0 + u * T;
+                    if (e < total) store_stream(kdst + int64_t(e) * 16, x[u]);
+                }
+            }
+        } else {
+            // V: transposed copy by VEC x VEC sub-blocks. Sub-block (kb, db)
+            // covers tokens kb*VEC .. +VEC-1 and dims db*VEC .. +VEC-1.
+            // Consecutive threads take consecutive db, so each load
+            // instruction reads whole token rows.
+            const char* vsrc = V + src;
+            char* vdst = Vp + int64_t(slot) * blk_bytes;
+            const int dblocks = d / VEC;
+            const int kblocks = block / VEC;
+            for (int e = tid; e < dblocks * kblocks; e += T) {
+                const int db = e % dblocks, kb = e / dblocks;
+                uint4 rows[VEC], cols[VEC];
+#pragma unroll
+                for (int r = 0; r < VEC; ++r) {
+                    const int t = kb * VEC + r;
+                    rows[r] = make_uint4(0, 0, 0, 0);
+                    if (t < cnt) rows[r] = load_stream(vsrc + (int64_t(t) * d + db * VEC) * ES);
+                }
+                if constexpr (BF16) transpose8x8_b16(rows, cols);
+                else transpose4x4_b32(rows, cols);
+                // cols[c] = dim db*VEC+c, tokens kb*VEC .. +VEC-1 -> V_packed[slot][dim][token]
+#pragma unroll
+                for (int c = 0; c < VEC; ++c)
+                    store_stream(vdst + (int64_t(db * VEC + c) * block + kb * VEC) * ES, cols[c]);
             }
         }
     }
@@ -190,13 +213,17 @@ hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void*
     offsets_kernel<<<g.H, 256, 0, s>>>(demand, g.H, g.n, g.W, head_off, slot_of, gather_blk);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    dim3 grid(g.n, g.H);
+    // One workgroup per CU walks the windows (measured best against 128..2048
+    // workgroups); the demand total is read on the device, so the grid is fixed.
+    const int grid = kGatherGrid;
     if (g.bf16)
-        gather_kernel<true><<<grid, 256, 0, s>>>(slot_of, (const char*)K, (const char*)V, (char*)Kp,
-                                                 (char*)Vp, g.L, g.d, g.block, g.n);
+        gather_kernel<true><<<grid, 256, 0, s>>>(head_off, gather_blk, (const char*)K,
+                                                 (const char*)V, (char*)Kp, (char*)Vp, g.H, g.L,
+                                                 g.d, g.block);
     else
-        gather_kernel<false><<<grid, 256, 0, s>>>(slot_of, (const char*)K, (const char*)V,
-                                                  (char*)Kp, (char*)Vp, g.L, g.d, g.block, g.n);
+        gather_kernel<false><<<grid, 256, 0, s>>>(head_off, gather_blk, (const char*)K,
+                                                  (const char*)V, (char*)Kp, (char*)Vp, g.H, g.L,
+                                                  g.d, g.block);
     return hipGetLastError();
 }
 

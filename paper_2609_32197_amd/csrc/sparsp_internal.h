@@ -13,6 +13,7 @@ namespace sparsp {
 constexpr int kMaxBlocks = 4096;        // n limit: 64 mask words per row
 constexpr int kMaxWords = kMaxBlocks / 64;
 constexpr int kMaxGlobal = 64;          // global (always-kept) blocks per call
+constexpr int kMaxHeads = 1024;         // H limit (head offsets are staged in LDS)
 
 // Derived geometry, computed once on the host.
 struct Geom {
