@@ -18,8 +18,7 @@ The computation follows the paper (arXiv 2609.32197):
   are packed row-major, each head a contiguous range, so that offsets can be
   derived locally on both ends.
 
-Readings taken where the paper is silent (each is listed with its reason in
-the design notes of the repository):
+Readings taken where the paper is silent:
 
 * pooling is the arithmetic mean over the valid tokens of a block;
 * the block score is the pooled dot product scaled by d**-0.5, rounded to
