@@ -237,6 +237,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         floatx16 s[C::MTW];
 #pragma unroll
         for (int mt = 0; mt < C::MTW; ++mt) s[mt] = floatx16{};
+        // The score MFMAs run at raised wave priority, so the matrix pipe is
+        // fed first while the SIMD's other wave fills in with softmax work.
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int kt = 0; kt < C::KT; ++kt) {
 #pragma unroll
@@ -247,6 +250,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kt], s[mt], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         if (cur & 1) {  // partial last block: keys past L do not exist
 #pragma unroll
             for (int mt = 0; mt < C::MTW; ++mt)

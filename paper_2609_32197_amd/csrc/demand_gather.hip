@@ -34,20 +34,27 @@ __device__ __forceinline__ void store_stream(char* p, uint4 v) {
     *reinterpret_cast<uint4*>(p) = v;
 }
 
+// Thread t ORs word t % W over the rows t / W, t / W + RG, ... (RG = 256 / W
+// row groups), so every thread has work even when a row is a few words.
 __global__ __launch_bounds__(256) void union_kernel(const uint64_t* __restrict__ mask, int nq,
                                                     int W, uint64_t* __restrict__ demand) {
-    __shared__ uint64_t part[4][64];
+    __shared__ uint64_t part[256];
     const int h = blockIdx.x;
-    const int w = threadIdx.x & 63;
-    const int rg = threadIdx.x >> 6;
+    const int tid = threadIdx.x;
+    const int rg_count = 256 / W;  // W <= 64, so at least 4 row groups
+    const int w = tid % W, rg = tid / W;
     uint64_t acc = 0;
-    if (w < W) {
+    if (rg < rg_count) {
         const uint64_t* m = mask + int64_t(h) * nq * W + w;
-        for (int i = rg; i < nq; i += 4) acc |= m[int64_t(i) * W];
+        for (int i = rg; i < nq; i += rg_count) acc |= m[int64_t(i) * W];
     }
-    part[rg][w] = acc;
+    part[tid] = acc;
     __syncthreads();
-    if (rg == 0 && w < W) demand[int64_t(h) * W + w] = part[0][w] | part[1][w] | part[2][w] | part[3][w];
+    if (tid < W) {
+        uint64_t r = 0;
+        for (int g = 0; g < rg_count; ++g) r |= part[g * W + tid];
+        demand[int64_t(h) * W + tid] = r;
+    }
 }
 
 __global__ __launch_bounds__(256) void offsets_kernel(const uint64_t* __restrict__ demand, int H,
@@ -121,8 +128,22 @@ __device__ __forceinline__ void transpose4x4_b32(const uint4 (&in)[4], uint4 (&o
     out[3] = make_uint4(in[0].w, in[1].w, in[2].w, in[3].w);
 }
 
-// The packed buffers are filled window by window: window 2s copies slot s's
-// K block, window 2s+1 writes its V block transposed. A grid-stride walk over
+constexpr int kMaxWS = 64;  // slots per window, at most
+
+// e / div for 0 <= e < 2^24 and div >= 1, with inv = 1.0f / div: the float
+// quotient is off by at most one, which the two corrections remove.
+__device__ __forceinline__ int div_small(int e, int div, float inv) {
+    int q = __float2int_rz(float(e) * inv);
+    if (q * div > e) --q;
+    if ((q + 1) * div <= e) ++q;
+    return q;
+}
+
+// The packed buffers are filled window by window. A window covers a group of
+// WS consecutive slots (WS > 1 only for small blocks, so that a window still
+// gives every thread work): window 2g copies the group's K blocks, window
+// 2g+1 writes its V blocks transposed. The group's source offsets and valid
+// row counts are looked up once per window into LDS. A grid-stride walk over
 // the windows keeps all resident workgroups on neighbouring slots, i.e. inside
 // one contiguous stretch of source and destination at any moment, which is
 // what lets the copy stream at full HBM rate; each thread keeps four 16-byte
@@ -133,43 +154,57 @@ __global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__
                                                      const char* __restrict__ K,
                                                      const char* __restrict__ V,
                                                      char* __restrict__ Kp, char* __restrict__ Vp,
-                                                     int H, int L, int d, int block) {
+                                                     int H, int L, int d, int block, int WS) {
     constexpr int ES = BF16 ? 2 : 4;  // element size
     constexpr int VEC = 16 / ES;      // elements per 16-byte chunk
     constexpr int T = 256;
     __shared__ int32_t hoff[kMaxHeads + 1];
+    __shared__ int64_t win_src[kMaxWS];  // byte offset of the block's first row in K and V
+    __shared__ int32_t win_cnt[kMaxWS];  // valid token rows of the block
     for (int i = threadIdx.x; i <= H; i += T) hoff[i] = head_off[i];
     __syncthreads();
     const int total_slots = hoff[H];
+    const int groups = (total_slots + WS - 1) / WS;
     const int64_t blk_bytes = int64_t(block) * d * ES;
     const int tid = threadIdx.x;
-    int h = 0;  // head of the current slot; slots only grow along the walk
-    for (int w = blockIdx.x; w < 2 * total_slots; w += gridDim.x) {
-        const int slot = w >> 1;
-        while (slot >= hoff[h + 1]) ++h;
-        const int j = gather_blk[slot];
-        const int tok0 = j * block;
-        const int cnt = min(block, L - tok0);
-        const int64_t src = (int64_t(h) * L + tok0) * d * ES;
+    const int row_chunks = d / VEC;             // 16-byte chunks per token row
+    const int k_items = block * row_chunks;     // chunks per K block
+    const int dblocks = d / VEC, kblocks = block / VEC;
+    const int v_items = dblocks * kblocks;      // VEC x VEC sub-blocks per V block
+    const float inv_k = 1.0f / float(k_items), inv_v = 1.0f / float(v_items);
+    int h = 0;  // this thread's table slot's head; its slots only grow along the walk
+    for (int w = blockIdx.x; w < 2 * groups; w += gridDim.x) {
+        const int s0 = (w >> 1) * WS;
+        const int ns = min(WS, total_slots - s0);
+        __syncthreads();  // the previous window is done with the table
+        if (tid < ns) {
+            const int slot = s0 + tid;
+            while (slot >= hoff[h + 1]) ++h;
+            const int tok0 = gather_blk[slot] * block;
+            win_src[tid] = (int64_t(h) * L + tok0) * d * ES;
+            win_cnt[tid] = min(block, L - tok0);
+        }
+        __syncthreads();
         if ((w & 1) == 0) {
-            // K: straight copy of `cnt` token rows, zero rows after.
-            const char* ksrc = K + src;
-            char* kdst = Kp + int64_t(slot) * blk_bytes;
-            const int row_chunks = d / VEC;
-            const int total = block * row_chunks;
-            const int valid = cnt * row_chunks;
+            // K: straight copy of the valid token rows, zero rows after.
+            const int total = ns * k_items;
             for (int e0 = tid; e0 < total; e0 += 4 * T) {
                 uint4 x[4];
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
                     const int e = e0 + u * T;
                     x[u] = make_uint4(0, 0, 0, 0);
-                    if (e < valid) x[u] = load_stream(ksrc + int64_t(e) * 16);
+                    if (e < total) {
+                        const int ls = WS == 1 ? 0 : div_small(e, k_items, inv_k);
+                        const int c = e - ls * k_items;
+                        if (c < win_cnt[ls] * row_chunks)
+                            x[u] = load_stream(K + win_src[ls] + int64_t(c) * 16);
+                    }
                 }
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
                     const int e = e0 + u * T;
-                    if (e < total) store_stream(kdst + int64_t(e) * 16, x[u]);
+                    if (e < total) store_stream(Kp + int64_t(s0) * blk_bytes + int64_t(e) * 16, x[u]);
                 }
             }
         } else {
@@ -177,18 +212,20 @@ __global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__
             // covers tokens kb*VEC .. +VEC-1 and dims db*VEC .. +VEC-1.
             // Consecutive threads take consecutive db, so each load
             // instruction reads whole token rows.
-            const char* vsrc = V + src;
-            char* vdst = Vp + int64_t(slot) * blk_bytes;
-            const int dblocks = d / VEC;
-            const int kblocks = block / VEC;
-            for (int e = tid; e < dblocks * kblocks; e += T) {
-                const int db = e % dblocks, kb = e / dblocks;
+            const int total = ns * v_items;
+            for (int e = tid; e < total; e += T) {
+                const int ls = WS == 1 ? 0 : div_small(e, v_items, inv_v);
+                const int r = e - ls * v_items;
+                const int db = r % dblocks, kb = r / dblocks;
+                const int cnt = win_cnt[ls];
+                const char* vsrc = V + win_src[ls];
+                char* vdst = Vp + int64_t(s0 + ls) * blk_bytes;
                 uint4 rows[VEC], cols[VEC];
 #pragma unroll
-                for (int r = 0; r < VEC; ++r) {
-                    const int t = kb * VEC + r;
-                    rows[r] = make_uint4(0, 0, 0, 0);
-                    if (t < cnt) rows[r] = load_stream(vsrc + (int64_t(t) * d + db * VEC) * ES);
+                for (int rr = 0; rr < VEC; ++rr) {
+                    const int t = kb * VEC + rr;
+                    rows[rr] = make_uint4(0, 0, 0, 0);
+                    if (t < cnt) rows[rr] = load_stream(vsrc + (int64_t(t) * d + db * VEC) * ES);
                 }
                 if constexpr (BF16) transpose8x8_b16(rows, cols);
                 else transpose4x4_b32(rows, cols);
@@ -216,14 +253,17 @@ hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void*
     // One workgroup per CU walks the windows (measured best against 128..2048
     // workgroups); the demand total is read on the device, so the grid is fixed.
     const int grid = kGatherGrid;
+    const int vec = g.bf16 ? 8 : 4;
+    const int v_items = (g.d / vec) * (g.block / vec);  // V sub-blocks per slot
+    const int ws = v_items >= 256 ? 1 : min(kMaxWS, (256 + v_items - 1) / v_items);
     if (g.bf16)
         gather_kernel<true><<<grid, 256, 0, s>>>(head_off, gather_blk, (const char*)K,
                                                  (const char*)V, (char*)Kp, (char*)Vp, g.H, g.L,
-                                                 g.d, g.block);
+                                                 g.d, g.block, ws);
     else
         gather_kernel<false><<<grid, 256, 0, s>>>(head_off, gather_blk, (const char*)K,
                                                   (const char*)V, (char*)Kp, (char*)Vp, g.H, g.L,
-                                                  g.d, g.block);
+                                                  g.d, g.block, ws);
     return hipGetLastError();
 }
 
