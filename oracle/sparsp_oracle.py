@@ -17,6 +17,11 @@ The computation follows the paper (arXiv 2609.32197):
 * Section 5.2: demand is kept per head (not unioned across heads) and blocks
   are packed row-major, each head a contiguous range, so that offsets can be
   derived locally on both ends.
+* Section 2.3 and Section 7: a rank attends to the KV shards of the owners
+  one at a time and combines the partial results with the online softmax;
+  Section 7.1 keeps the local shard whole and cuts the last remote shard into
+  finer chunks; Section 7.2 cuts shards into chunks of heads and runs the
+  sparsest chunk last.
 
 Readings taken where the paper is silent:
 
@@ -30,7 +35,14 @@ Readings taken where the paper is silent:
 * demand packs every demanded block, local and remote; the remote part is
   what Eq. 3 counts;
 * the packed K buffer keeps each block as [block, d]; the packed V buffer
-  stores each block transposed, [d, block]; token rows past L are zero.
+  stores each block transposed, [d, block]; token rows past L are zero;
+* a chunk is (owner shard, run of consecutive heads); shards are taken in
+  ring order from the local one (r, r+1, ..., r+R-1 mod R); remote shards are
+  cut into chunks of a given number of heads, the last remote shard into
+  chunks of a second, smaller number; inside each remote shard, chunks run
+  in order of selected blocks descending (the heads' demanded blocks in that
+  shard), ties by head, so that the sparsest chunk of the last shard ends the
+  pipeline.
 
 Precision: every arithmetic step is float64; the float32 block scores are the
 hand-off value for selection. Attention is evaluated directly from Q, K, V
@@ -65,6 +77,11 @@ __all__ = [
     "dense_attention",
     "attention_flops",
     "exchange_volume",
+    "owner_ranges",
+    "attend_part",
+    "lse_merge",
+    "chunk_plan",
+    "chunked_attention",
 ]
 
 
@@ -363,3 +380,119 @@ def exchange_volume(demand: np.ndarray, ranks: int, rank: int, block: int, d: in
         owner[lo:hi] = p
     remote = demand & (owner[None, :] != rank)
     return int(2 * block * d * w * remote.sum())
+
+
+# ---------------------------------------------------------------------------
+# Section 2.3 and Section 7: attention shard by shard, chunks of heads, and the
+# online-softmax merge of the partial results
+# ---------------------------------------------------------------------------
+
+def owner_ranges(n: int, ranks: int) -> list:
+    """[(lo, hi)] per owner p: the contiguous blocks [floor(p n / R), floor((p+1) n / R))."""
+    return [local_range(n, ranks, p) for p in range(ranks)]
+
+
+def attend_part(Qh: np.ndarray, Kh: np.ndarray, Vh: np.ndarray, mask_row: np.ndarray, i: int,
+                L: int, block: int, scale: float, kv_range: tuple):
+    """Attention of query block i over the kept blocks that lie in [lo, hi) only.
+
+    The softmax and its log-sum-exp run over that part of the kept keys alone.
+    Rows with no kept key in the range get O = 0 and lse = -inf, the identity
+    of the merge below.
+    """
+    lo, hi = kv_range
+    part = mask_row.copy()
+    part[:lo] = False
+    part[hi:] = False
+    d = Qh.shape[1]
+    if not part.any():
+        return np.zeros((block, d)), np.full(block, -np.inf)
+    return attend_block(Qh, Kh, Vh, part, i, L, block, scale)
+
+
+def lse_merge(O_a: np.ndarray, lse_a: np.ndarray, O_b: np.ndarray, lse_b: np.ndarray) -> tuple:
+    """Softmax results over two disjoint key sets A and B -> the result over A u B.
+
+    With Z_X = exp(lse_X) the softmax denominator over X and O_X its weighted
+    mean of V: O = (Z_A O_A + Z_B O_B) / (Z_A + Z_B), lse = log(Z_A + Z_B),
+    evaluated relative to m = max(lse_A, lse_B). A row with lse = -inf on one
+    side takes the other side unchanged; on both sides it stays O = 0, -inf.
+    Shapes: O [..., d], lse [...].
+    """
+    m = np.maximum(lse_a, lse_b)
+    finite = np.isfinite(m)
+    m_safe = np.where(finite, m, 0.0)
+    w_a = np.where(np.isfinite(lse_a), np.exp(lse_a - m_safe), 0.0)
+    w_b = np.where(np.isfinite(lse_b), np.exp(lse_b - m_safe), 0.0)
+    tot = w_a + w_b
+    safe = np.where(finite, tot, 1.0)
+    O = np.where(finite[..., None], (w_a[..., None] * O_a + w_b[..., None] * O_b) / safe[..., None],
+                 0.0)
+    lse = np.where(finite, m_safe + np.log(safe), -np.inf)
+    return O, lse
+
+
+def chunk_plan(demand: np.ndarray, ranks: int, rank: int, heads_per_chunk: int,
+               tail_heads_per_chunk: int) -> list:
+    """Chunk schedule of rank r's attention (Section 7.1, Section 7.2).
+
+    demand: bool [H, n]. Returns [(owner, lo, hi, h_begin, h_end, blocks)] in
+    execution order: the local shard (owner r, all heads) first, then the
+    remote shards in ring order r+1, ..., r+R-1 (mod R). A remote shard is cut
+    into runs of heads_per_chunk heads (the last one of the pipeline into runs
+    of tail_heads_per_chunk), and its chunks run by selected blocks
+    descending, then head ascending. `blocks` counts the demanded blocks of
+    the chunk's heads inside the shard.
+    """
+    H, n = demand.shape
+    if heads_per_chunk < 1 or tail_heads_per_chunk < 1:
+        raise ValueError("chunk sizes must be positive")
+    if not 0 <= rank < ranks:
+        raise ValueError("rank out of range")
+    rng = owner_ranges(n, ranks)
+    plan = []
+    lo, hi = rng[rank]
+    plan.append((rank, lo, hi, 0, H, int(demand[:, lo:hi].sum())))
+    for k in range(1, ranks):
+        p = (rank + k) % ranks
+        lo, hi = rng[p]
+        size = tail_heads_per_chunk if k == ranks - 1 else heads_per_chunk
+        chunks = []
+        for h0 in range(0, H, size):
+            h1 = min(H, h0 + size)
+            chunks.append((p, lo, hi, h0, h1, int(demand[h0:h1, lo:hi].sum())))
+        chunks.sort(key=lambda c: (-c[5], c[3]))
+        plan.extend(chunks)
+    return plan
+
+
+def chunked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, mask: np.ndarray, L: int,
+                      block: int, i0: int, scale: float, plan: Sequence[tuple],
+                      pairs: Optional[Iterable[tuple]] = None) -> tuple:
+    """Block-sparse attention evaluated chunk by chunk in `plan` order and merged.
+
+    Every chunk attends the query blocks of its heads to the kept blocks inside
+    its shard (attend_part) and is folded into the running result with
+    lse_merge. With ``pairs`` only those (h, local row) query blocks are
+    evaluated; the rest of O and lse are NaN.
+    """
+    H, nq, n = mask.shape
+    d = Q.shape[2]
+    want = set(pairs) if pairs is not None else None
+    O = np.zeros((H, nq * block, d))
+    LSE = np.full((H, nq * block), -np.inf)
+    for (_, lo, hi, h0, h1, _) in plan:
+        for h in range(h0, h1):
+            for r in range(nq):
+                if want is not None and (h, r) not in want:
+                    continue
+                rows = slice(r * block, (r + 1) * block)
+                o, l = attend_part(Q[h], K[h], V[h], mask[h, r], i0 + r, L, block, scale, (lo, hi))
+                O[h, rows], LSE[h, rows] = lse_merge(O[h, rows], LSE[h, rows], o, l)
+    if want is not None:
+        keep_rows = np.zeros((H, nq * block), dtype=bool)
+        for h, r in want:
+            keep_rows[h, r * block:(r + 1) * block] = True
+        O[~keep_rows] = np.nan
+        LSE[~keep_rows] = np.nan
+    return O, LSE
