@@ -50,6 +50,12 @@ def parse_args(argv=None):
                     help="wall-clock budget of the oracle sample")
     ap.add_argument("--cache-dir", default=None,
                     help="keep generated inputs as .npy files here and reuse them")
+    ap.add_argument("--chunk-heads", type=int, default=8,
+                    help="heads per chunk of a remote shard (shard-by-shard attention)")
+    ap.add_argument("--tail-chunk-heads", type=int, default=2,
+                    help="heads per chunk of the last remote shard")
+    ap.add_argument("--no-extensions", action="store_true",
+                    help="skip the shard-by-shard attention measurement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of this many MiB (for counter calibration)")
     return ap.parse_args(argv)
@@ -160,6 +166,71 @@ def cpu_baseline(wl, q, k, v, budget_s):
         "kind": "oracle",
         "sample": f"{heads} of {wl.H} heads, whole pipeline (pool, score, select, union, pack, "
                   f"attend) per head, {spent:.1f} s",
+    }
+
+
+def time_calls(fn, reps, stream):
+    """Mean milliseconds of fn() over reps calls, HIP events on `stream`, after one warm call."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def measure_chunked(sp, g, wl, Q, bufs, packed, stream, a):
+    """Shard-by-shard attention of this rank (Section 2.3, Section 7): the chunk
+    schedule run with sparsp_chunked_attn against one unchunked call with the
+    same float32 output, and the log-sum-exp merge on its own over every head."""
+    import torch
+    plan = sp.sparsp_chunk_plan(g, packed["demand"], wl.ranks, wl.rank, a.chunk_heads,
+                                a.tail_chunk_heads)
+    f32 = torch.float32
+    so, sl = (wl.H, wl.nq * wl.block, wl.d), (wl.H, wl.nq * wl.block)
+    O, lse, Op, lp = (torch.empty(x, dtype=f32, device="cuda") for x in (so, sl, so, sl))
+    reps = 5
+
+    def chunked():
+        sp.sparsp_chunked_attn(g, Q, bufs["sel"], packed["slot_of"], packed["K_packed"],
+                               packed["V_packed"], plan, wl.softmax_scale, O=O, lse=lse,
+                               stream=stream)
+
+    def whole():
+        sp.sparsp_block_sparse_attn(g, Q, bufs["sel"], packed["slot_of"], packed["K_packed"],
+                                    packed["V_packed"], wl.softmax_scale, out_dtype=sp.F32, O=Op,
+                                    lse=lp, stream=stream)
+
+    def merge():
+        sp.sparsp_lse_merge(g, (0, wl.H), O, lse, Op, lp, stream=stream)
+
+    c0 = plan[0]
+
+    def local():
+        sp.sparsp_block_sparse_attn_part(g, Q, bufs["sel"], packed["slot_of"], packed["K_packed"],
+                                         packed["V_packed"], (c0.kv_blk_begin, c0.kv_blk_end),
+                                         (c0.head_begin, c0.head_end), wl.softmax_scale, O=Op,
+                                         lse=lp, stream=stream)
+
+    t_chunked = time_calls(chunked, reps, stream)
+    t_local = time_calls(local, reps, stream)
+    t_whole = time_calls(whole, reps, stream)
+    t_merge = time_calls(merge, reps, stream)
+    rows = wl.H * wl.nq * wl.block
+    mbytes = rows * (12 * wl.d + 12)  # read both O and lse, write the accumulator
+    return {
+        "ranks": wl.ranks, "rank": wl.rank, "heads_per_chunk": a.chunk_heads,
+        "tail_heads_per_chunk": a.tail_chunk_heads, "chunks": len(plan),
+        "chunked_ms": t_chunked, "local_shard_ms": t_local,
+        "remote_chunks_ms": t_chunked - t_local, "unchunked_f32_out_ms": t_whole,
+        "overhead_frac": t_chunked / t_whole - 1.0,
+        "merge": {"rows": rows, "ms": t_merge, "algorithmic_bytes": mbytes,
+                  "GBps": mbytes / (t_merge * 1e-3) / 1e9,
+                  "frac_of_hbm_peak": mbytes / (t_merge * 1e-3) / 1e9 / PEAK_HBM_GBPS},
     }
 
 
@@ -304,6 +375,11 @@ def main(argv=None) -> int:
         },
         "cpu_baseline": None,
     }
+    if not a.no_extensions and wl.ranks > 1:
+        rec["chunked_attention"] = measure_chunked(sp, g, wl, Q, bufs, packed, stream, a)
+        c = rec["chunked_attention"]
+        log(f"[bench] shard-by-shard: {c['chunks']} chunks {c['chunked_ms']:.3f} ms vs "
+            f"{c['unchunked_f32_out_ms']:.3f} ms unchunked; merge {c['merge']['GBps']:.0f} GB/s")
     log(f"[bench] {wl.name}: {ms_per_step:.3f} ms/layer, attention {stage_ms['block_sparse_attn']:.3f} ms "
         f"= {attn_tflops:.0f} TFLOP/s ({100 * attn_tflops / peak:.1f}% of peak), stages {stage_ms}")
     if not a.no_cpu_baseline:

@@ -147,6 +147,91 @@ int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t*
                              const void* V_packed, int64_t capacity_blocks, float softmax_scale,
                              void* O, int32_t out_dtype, float* lse, void* stream);
 
+/*
+ * Shard-by-shard attention (Section 2.3: a rank attends to one owner's KV
+ * shard at a time and folds the partial result in with the online softmax;
+ * Section 7: shards are cut into chunks of heads and ordered to shorten the
+ * pipeline tail). Owner p of R holds the blocks [floor(p n / R),
+ * floor((p+1) n / R)). Chunk results are float32.
+ */
+
+/* One chunk of a schedule. */
+typedef struct {
+    int32_t owner;        /* rank that owns the shard */
+    int32_t kv_blk_begin; /* the shard: blocks [kv_blk_begin, kv_blk_end) */
+    int32_t kv_blk_end;
+    int32_t head_begin;   /* the chunk's heads [head_begin, head_end) */
+    int32_t head_end;
+    int32_t blocks;       /* demanded blocks of those heads inside the shard */
+} sparsp_chunk;
+
+/*
+ * The chunk schedule of rank `rank` of `ranks` (Section 7.1, Section 7.2):
+ * the local shard first, whole (all heads); then the remote shards in ring
+ * order rank+1, ..., rank+ranks-1 (mod ranks), each cut into runs of
+ * heads_per_chunk consecutive heads, the last one into runs of
+ * tail_heads_per_chunk heads; inside each remote shard the chunks run by
+ * `blocks` descending, then head_begin ascending, so the sparsest chunk ends
+ * the pipeline.
+ *
+ * demand: HOST uint64 [H, W] as written by sparsp_demand_union_gather (copy it
+ * back first). chunks: HOST array of max_chunks entries. Returns the number of
+ * chunks written (>= 1), SPARSP_E_CAPACITY if max_chunks is too small (the
+ * message gives the count needed; 1 + (ranks-1) * ceil(H / min chunk size)
+ * always suffices), or SPARSP_E_INVALID for ranks outside [1, n], rank
+ * outside [0, ranks), a chunk size below 1 or a NULL pointer. Pure host code.
+ */
+int sparsp_chunk_plan(const sparsp_geom* g, const uint64_t* demand, int32_t ranks, int32_t rank,
+                      int32_t heads_per_chunk, int32_t tail_heads_per_chunk, sparsp_chunk* chunks,
+                      int32_t max_chunks);
+
+/*
+ * Attention of the local query blocks of heads [head_begin, head_end) over
+ * the kept blocks that lie inside [kv_blk_begin, kv_blk_end) only: Step 4
+ * restricted to one shard and one chunk of heads. The softmax and lse run over
+ * those keys alone. Arguments as for sparsp_block_sparse_attn, except that O
+ * is float32 [H, nq*block, d] and lse float32 [H, nq*block] is required; only
+ * the rows of the chunk's heads are touched. 0 <= kv_blk_begin <= kv_blk_end
+ * <= n and 0 <= head_begin < head_end <= H.
+ *
+ * accumulate == 0: (O, lse) are overwritten with the part's result; a row with
+ * no kept key in the part gets O = 0, lse = -inf (the merge identity).
+ * accumulate != 0: (O, lse) hold a running result (from an earlier call, or
+ * O = 0 and lse = -inf) and the part is folded into it exactly as
+ * sparsp_lse_merge would; rows with no kept key in the part are left as they
+ * are, and query blocks with none are not read or written at all.
+ */
+int sparsp_block_sparse_attn_part(const sparsp_geom* g, const void* Q, const int32_t* sel,
+                                  int32_t keep, const int32_t* slot_of, const void* K_packed,
+                                  const void* V_packed, int64_t capacity_blocks,
+                                  float softmax_scale, int32_t kv_blk_begin, int32_t kv_blk_end,
+                                  int32_t head_begin, int32_t head_end, float* O, float* lse,
+                                  int32_t accumulate, void* stream);
+
+/*
+ * Folds a part (O_part, lse_part) into the accumulator (O_acc, lse_acc), in
+ * place, for the rows of heads [head_begin, head_end): with m the larger lse
+ * and w = exp(lse - m) per side, O = (w_a O_a + w_b O_b) / (w_a + w_b) and
+ * lse = m + log(w_a + w_b); a side with lse = -inf contributes nothing. All
+ * four are float32, O [H, nq*block, d], lse [H, nq*block], 16-byte aligned;
+ * the part may not alias the accumulator.
+ */
+int sparsp_lse_merge(const sparsp_geom* g, int32_t head_begin, int32_t head_end, float* O_acc,
+                     float* lse_acc, const float* O_part, const float* lse_part, void* stream);
+
+/*
+ * Runs a schedule on `stream`, one attention launch per chunk in plan order: a
+ * chunk whose heads have no result yet writes (O, lse) (accumulate = 0), every
+ * other chunk is folded in (accumulate = 1); heads that no chunk covers end
+ * with O = 0, lse = -inf. plan: HOST array of n_chunks chunks (each range
+ * checked as above). O float32 [H, nq*block, d], lse float32 [H, nq*block].
+ * Allocates nothing.
+ */
+int sparsp_chunked_attn(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t keep,
+                        const int32_t* slot_of, const void* K_packed, const void* V_packed,
+                        int64_t capacity_blocks, float softmax_scale, const sparsp_chunk* plan,
+                        int32_t n_chunks, float* O, float* lse, void* stream);
+
 /* Message of the calling thread's most recent error ("" if none). */
 const char* sparsp_last_error(void);
 

@@ -11,6 +11,13 @@ a tensor is not on the GPU, the call raises.
     sparsp_demand_union_gather  per-head demand (Eq. 2) and packed K/V (Section 5.2)
     sparsp_block_sparse_attn    attention of the local query blocks (Eq. 1)
 
+Shard-by-shard attention (Section 2.3, Section 7):
+
+    sparsp_chunk_plan              the chunk schedule of one rank (host)
+    sparsp_block_sparse_attn_part  attention over one shard for a run of heads
+    sparsp_lse_merge               online-softmax merge of two partial results
+    sparsp_chunked_attn            a whole schedule, attended and merged
+
 Short aliases without the prefix are provided as well.
 """
 
@@ -37,6 +44,15 @@ __all__ = [
     "topk_mask",
     "demand_union_gather",
     "block_sparse_attn",
+    "Chunk",
+    "sparsp_chunk_plan",
+    "sparsp_block_sparse_attn_part",
+    "sparsp_lse_merge",
+    "sparsp_chunked_attn",
+    "chunk_plan",
+    "block_sparse_attn_part",
+    "lse_merge",
+    "chunked_attn",
     "F32",
     "BF16",
     "STATUS",
@@ -96,7 +112,20 @@ class Geometry:
         return _Geom(self.H, self.L, self.d, self.block, self.i0, self.i1, self.dtype)
 
 
+class Chunk(ctypes.Structure):
+    """sparsp_chunk: shard [kv_blk_begin, kv_blk_end) of `owner`, heads [head_begin, head_end)."""
+
+    _fields_ = [("owner", ctypes.c_int32), ("kv_blk_begin", ctypes.c_int32),
+                ("kv_blk_end", ctypes.c_int32), ("head_begin", ctypes.c_int32),
+                ("head_end", ctypes.c_int32), ("blocks", ctypes.c_int32)]
+
+    def astuple(self) -> tuple:
+        return (self.owner, self.kv_blk_begin, self.kv_blk_end, self.head_begin, self.head_end,
+                self.blocks)
+
+
 _VP = ctypes.c_void_p
+_I32 = ctypes.c_int32
 _SIGNATURES = {
     "sparsp_block_scores": [ctypes.POINTER(_Geom), _VP, _VP, _VP, _VP, _VP, _VP],
     "sparsp_topk_mask": [ctypes.POINTER(_Geom), _VP, ctypes.c_int32,
@@ -105,6 +134,14 @@ _SIGNATURES = {
                                    _VP, _VP, ctypes.c_int64, _VP],
     "sparsp_block_sparse_attn": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP, _VP, _VP,
                                  ctypes.c_int64, ctypes.c_float, _VP, ctypes.c_int32, _VP, _VP],
+    "sparsp_chunk_plan": [ctypes.POINTER(_Geom), _VP, _I32, _I32, _I32, _I32,
+                          ctypes.POINTER(Chunk), _I32],
+    "sparsp_block_sparse_attn_part": [ctypes.POINTER(_Geom), _VP, _VP, _I32, _VP, _VP, _VP,
+                                      ctypes.c_int64, ctypes.c_float, _I32, _I32, _I32, _I32,
+                                      _VP, _VP, _I32, _VP],
+    "sparsp_lse_merge": [ctypes.POINTER(_Geom), _I32, _I32, _VP, _VP, _VP, _VP, _VP],
+    "sparsp_chunked_attn": [ctypes.POINTER(_Geom), _VP, _VP, _I32, _VP, _VP, _VP, ctypes.c_int64,
+                            ctypes.c_float, ctypes.POINTER(Chunk), _I32, _VP, _VP, _VP],
 }
 
 
@@ -136,7 +173,7 @@ def version() -> int:
 
 
 def _check(rc: int):
-    if rc != 0:
+    if rc < 0:
         msg = load_library().sparsp_last_error().decode(errors="replace")
         raise SparspError(rc, msg)
 
@@ -299,7 +336,121 @@ def sparsp_block_sparse_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed
     return o, ls
 
 
+# ---------------------------------------------------------------------------
+# shard-by-shard attention
+# ---------------------------------------------------------------------------
+
+def sparsp_chunk_plan(geom: Geometry, demand, ranks: int, rank: int, heads_per_chunk: int,
+                      tail_heads_per_chunk: int) -> list:
+    """The chunk schedule of rank `rank` (host). demand: [H, W] uint64 bits (any device).
+
+    Returns a list of Chunk structures in execution order.
+    """
+    import numpy as np
+    g = geom
+    if hasattr(demand, "detach"):
+        demand = demand.detach().cpu().numpy()
+    dem = np.ascontiguousarray(np.asarray(demand).view(np.uint64).reshape(g.H, g.W))
+    cap = 1 + max(0, int(ranks) - 1) * g.H
+    arr = (Chunk * cap)()
+    gs = g.c_struct()
+    rc = load_library().sparsp_chunk_plan(ctypes.byref(gs), dem.ctypes.data, int(ranks), int(rank),
+                                          int(heads_per_chunk), int(tail_heads_per_chunk), arr, cap)
+    _check(rc)
+    return [Chunk(*arr[i].astuple()) for i in range(rc)]
+
+
+def _packed_args(g, K_packed, V_packed, et):
+    if K_packed.dim() != 3 or V_packed.dim() != 3:
+        raise ValueError("K_packed and V_packed must be 3-D")
+    cap = int(K_packed.shape[0])
+    if tuple(K_packed.shape[1:]) != (g.block, g.d) or tuple(V_packed.shape) != (cap, g.d, g.block):
+        raise ValueError("packed buffers must be [cap, block, d] and [cap, d, block]")
+    return _dev(K_packed, "K_packed", et), _dev(V_packed, "V_packed", et), ctypes.c_int64(cap)
+
+
+def _scale(g, softmax_scale):
+    if softmax_scale is None:
+        softmax_scale = ctypes.c_float(1.0 / math.sqrt(g.d)).value
+    return ctypes.c_float(softmax_scale)
+
+
+def sparsp_block_sparse_attn_part(geom: Geometry, Q, sel, slot_of, K_packed, V_packed,
+                                  kv_blocks: tuple, heads: tuple,
+                                  softmax_scale: Optional[float] = None, O=None, lse=None,
+                                  accumulate: bool = False, stream=None):
+    """Attention over the kept blocks in kv_blocks = (lo, hi) for heads = (h0, h1).
+
+    Returns (O float32 [H, nq*block, d], lse float32 [H, nq*block]); only the
+    rows of heads h0..h1-1 are touched. With accumulate, (O, lse) must be given
+    and hold a running result that the part is folded into.
+    """
+    if accumulate and (O is None or lse is None):
+        raise ValueError("accumulate needs the running (O, lse)")
+    torch = _torch()
+    g = geom
+    et = _elem_dtype(g)
+    keep = int(sel.shape[-1])
+    o = O if O is not None else _empty((g.H, g.nq * g.block, g.d), torch.float32, Q)
+    ls = lse if lse is not None else _empty((g.H, g.nq * g.block), torch.float32, Q)
+    kp, vp, cap = _packed_args(g, K_packed, V_packed, et)
+    args = (
+        _dev(Q, "Q", et, (g.H, g.L, g.d)), _dev(sel, "sel", torch.int32, (g.H, g.nq, keep)),
+        ctypes.c_int32(keep), _dev(slot_of, "slot_of", torch.int32, (g.H, g.n)), kp, vp, cap,
+        _scale(g, softmax_scale), int(kv_blocks[0]), int(kv_blocks[1]), int(heads[0]),
+        int(heads[1]), _dev(o, "O", torch.float32, (g.H, g.nq * g.block, g.d)),
+        _dev(ls, "lse", torch.float32, (g.H, g.nq * g.block)), int(bool(accumulate)),
+    )
+    gs = g.c_struct()
+    _check(load_library().sparsp_block_sparse_attn_part(ctypes.byref(gs), *args,
+                                                       _stream(stream, Q.device)))
+    return o, ls
+
+
+def sparsp_lse_merge(geom: Geometry, heads: tuple, O_acc, lse_acc, O_part, lse_part, stream=None):
+    """Folds (O_part, lse_part) into (O_acc, lse_acc) in place for heads (h0, h1)."""
+    torch = _torch()
+    g = geom
+    so, sl = (g.H, g.nq * g.block, g.d), (g.H, g.nq * g.block)
+    args = (
+        int(heads[0]), int(heads[1]),
+        _dev(O_acc, "O_acc", torch.float32, so), _dev(lse_acc, "lse_acc", torch.float32, sl),
+        _dev(O_part, "O_part", torch.float32, so), _dev(lse_part, "lse_part", torch.float32, sl),
+    )
+    gs = g.c_struct()
+    _check(load_library().sparsp_lse_merge(ctypes.byref(gs), *args, _stream(stream, O_acc.device)))
+    return O_acc, lse_acc
+
+
+def sparsp_chunked_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed, plan: Sequence,
+                        softmax_scale: Optional[float] = None, O=None, lse=None, stream=None):
+    """Runs a chunk schedule (a list of Chunk or 6-tuples). Returns (O, lse), float32."""
+    torch = _torch()
+    g = geom
+    et = _elem_dtype(g)
+    keep = int(sel.shape[-1])
+    so, sl = (g.H, g.nq * g.block, g.d), (g.H, g.nq * g.block)
+    o = O if O is not None else _empty(so, torch.float32, Q)
+    ls = lse if lse is not None else _empty(sl, torch.float32, Q)
+    chunks = [c if isinstance(c, Chunk) else Chunk(*[int(x) for x in c]) for c in plan]
+    arr = (Chunk * max(1, len(chunks)))(*chunks)
+    kp, vp, cap = _packed_args(g, K_packed, V_packed, et)
+    args = (
+        _dev(Q, "Q", et, (g.H, g.L, g.d)), _dev(sel, "sel", torch.int32, (g.H, g.nq, keep)),
+        ctypes.c_int32(keep), _dev(slot_of, "slot_of", torch.int32, (g.H, g.n)), kp, vp, cap,
+        _scale(g, softmax_scale), arr, len(chunks),
+        _dev(o, "O", torch.float32, so), _dev(ls, "lse", torch.float32, sl),
+    )
+    gs = g.c_struct()
+    _check(load_library().sparsp_chunked_attn(ctypes.byref(gs), *args, _stream(stream, Q.device)))
+    return o, ls
+
+
 block_scores = sparsp_block_scores
 topk_mask = sparsp_topk_mask
 demand_union_gather = sparsp_demand_union_gather
 block_sparse_attn = sparsp_block_sparse_attn
+chunk_plan = sparsp_chunk_plan
+block_sparse_attn_part = sparsp_block_sparse_attn_part
+lse_merge = sparsp_lse_merge
+chunked_attn = sparsp_chunked_attn

@@ -78,11 +78,46 @@ int check_chunked(const sparsp::Geom& G) {
     return SPARSP_OK;
 }
 
+// Checks shared by every attention entry point (not the output buffers).
+int check_attn(const sparsp::Geom& G, const void* Q, const int32_t* sel, int keep,
+               const int32_t* slot_of, const void* Kp, const void* Vp, int64_t capacity,
+               float scale) {
+    if (!Q || !sel || !slot_of || !Kp || !Vp) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (keep < 1 || keep > G.n)
+        return fail(SPARSP_E_INVALID, "keep = %d outside [1, n = %d]", keep, G.n);
+    if (capacity < 1) return fail(SPARSP_E_CAPACITY, "capacity_blocks < 1");
+    if (int rc = check_chunked(G)) return rc;
+    if (!aligned16(Q) || !aligned16(Kp) || !aligned16(Vp))
+        return fail(SPARSP_E_INVALID, "Q and the packed buffers must be 16-byte aligned");
+    if (!(scale > 0.0f) || scale > 1e30f)
+        return fail(SPARSP_E_INVALID, "softmax_scale must be positive and finite");
+    if (G.bf16) {
+        const bool ok_shape = (G.d == 64 || G.d == 128) && (G.block == 64 || G.block == 128);
+        if (!ok_shape)
+            return fail(SPARSP_E_UNSUPPORTED,
+                        "bf16 attention needs d and block in {64, 128} (d=%d block=%d)", G.d,
+                        G.block);
+    } else if (G.d > 128 || G.block > 256) {
+        return fail(SPARSP_E_UNSUPPORTED, "f32 attention needs d <= 128 and block <= 256");
+    }
+    return SPARSP_OK;
+}
+
+// A shard [kv_lo, kv_hi) of blocks and a run [h_lo, h_hi) of heads.
+int check_part(const sparsp::Geom& G, int kv_lo, int kv_hi, int h_lo, int h_hi) {
+    if (kv_lo < 0 || kv_hi > G.n || kv_lo > kv_hi)
+        return fail(SPARSP_E_INVALID, "block range [%d, %d) not inside [0, %d]", kv_lo, kv_hi, G.n);
+    if (h_lo < 0 || h_hi > G.H || h_lo >= h_hi)
+        return fail(SPARSP_E_INVALID, "head range [%d, %d) not inside [0, %d) or empty", h_lo,
+                    h_hi, G.H);
+    return SPARSP_OK;
+}
+
 }  // namespace
 
 extern "C" {
 
-int sparsp_version(void) { return 100; }  // 0.1.0
+int sparsp_version(void) { return 200; }  // 0.2.0
 
 const char* sparsp_last_error(void) { return g_err; }
 
@@ -159,37 +194,112 @@ int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t*
                              int32_t out_dtype, float* lse, void* stream) {
     sparsp::Geom G;
     if (int rc = derive(g, &G)) return rc;
-    if (!Q || !sel || !slot_of || !K_packed || !V_packed || !O)
-        return fail(SPARSP_E_INVALID, "NULL tensor pointer");
-    if (keep < 1 || keep > G.n)
-        return fail(SPARSP_E_INVALID, "keep = %d outside [1, n = %d]", keep, G.n);
-    if (capacity_blocks < 1) return fail(SPARSP_E_CAPACITY, "capacity_blocks < 1");
-    if (int rc = check_chunked(G)) return rc;
-    if (!aligned16(Q) || !aligned16(K_packed) || !aligned16(V_packed) || !aligned16(O))
-        return fail(SPARSP_E_INVALID, "Q, O and the packed buffers must be 16-byte aligned");
-    if (!(softmax_scale > 0.0f) || softmax_scale > 1e30f)
-        return fail(SPARSP_E_INVALID, "softmax_scale must be positive and finite");
+    if (!O) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (int rc = check_attn(G, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                            softmax_scale))
+        return rc;
+    if (!aligned16(O)) return fail(SPARSP_E_INVALID, "O must be 16-byte aligned");
     if (out_dtype != SPARSP_F32 && out_dtype != SPARSP_BF16)
         return fail(SPARSP_E_DTYPE, "unknown out_dtype %d", out_dtype);
+    if (!G.bf16 && out_dtype != SPARSP_F32)
+        return fail(SPARSP_E_DTYPE, "f32 inputs produce f32 output only");
+    const sparsp::AttnPart whole{0, G.n, 0, G.H, 0};
     hipStream_t s = (hipStream_t)stream;
-    hipError_t e;
-    if (G.bf16) {
-        const bool ok_shape = (G.d == 64 || G.d == 128) && (G.block == 64 || G.block == 128);
-        if (!ok_shape)
-            return fail(SPARSP_E_UNSUPPORTED, "bf16 attention needs d and block in {64, 128} (d=%d block=%d)",
-                        G.d, G.block);
-        e = sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
-                                     softmax_scale, O, out_dtype == SPARSP_BF16, lse, s);
-    } else {
-        if (out_dtype != SPARSP_F32)
-            return fail(SPARSP_E_DTYPE, "f32 inputs produce f32 output only");
-        if (G.d > 128 || G.block > 256)
-            return fail(SPARSP_E_UNSUPPORTED, "f32 attention needs d <= 128 and block <= 256");
-        e = sparsp::launch_attn_f32(G, (const float*)Q, sel, keep, slot_of, (const float*)K_packed,
-                                    (const float*)V_packed, capacity_blocks, softmax_scale,
-                                    (float*)O, lse, s);
-    }
+    hipError_t e =
+        G.bf16 ? sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed,
+                                          capacity_blocks, softmax_scale, whole, O,
+                                          out_dtype == SPARSP_BF16, lse, s)
+               : sparsp::launch_attn_f32(G, (const float*)Q, sel, keep, slot_of,
+                                         (const float*)K_packed, (const float*)V_packed,
+                                         capacity_blocks, softmax_scale, whole, (float*)O, lse, s);
     return hip_status(e, "sparsp_block_sparse_attn");
+}
+
+int sparsp_chunk_plan(const sparsp_geom* g, const uint64_t* demand, int32_t ranks, int32_t rank,
+                      int32_t heads_per_chunk, int32_t tail_heads_per_chunk, sparsp_chunk* chunks,
+                      int32_t max_chunks) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!demand || !chunks) return fail(SPARSP_E_INVALID, "NULL pointer");
+    if (ranks < 1 || ranks > G.n)
+        return fail(SPARSP_E_INVALID, "ranks = %d outside [1, n = %d]", ranks, G.n);
+    if (rank < 0 || rank >= ranks)
+        return fail(SPARSP_E_INVALID, "rank = %d outside [0, %d)", rank, ranks);
+    if (heads_per_chunk < 1 || tail_heads_per_chunk < 1)
+        return fail(SPARSP_E_INVALID, "chunk sizes must be at least one head");
+    if (max_chunks < 0) return fail(SPARSP_E_INVALID, "max_chunks < 0");
+    const int r = sparsp::plan_chunks(G, demand, ranks, rank, heads_per_chunk,
+                                      tail_heads_per_chunk, chunks, max_chunks);
+    if (r < 0)
+        return fail(SPARSP_E_CAPACITY, "the schedule has %d chunks, max_chunks = %d", -r,
+                    max_chunks);
+    ok();
+    return r;
+}
+
+int sparsp_block_sparse_attn_part(const sparsp_geom* g, const void* Q, const int32_t* sel,
+                                  int32_t keep, const int32_t* slot_of, const void* K_packed,
+                                  const void* V_packed, int64_t capacity_blocks,
+                                  float softmax_scale, int32_t kv_blk_begin, int32_t kv_blk_end,
+                                  int32_t head_begin, int32_t head_end, float* O, float* lse,
+                                  int32_t accumulate, void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!O || !lse) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (int rc = check_attn(G, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                            softmax_scale))
+        return rc;
+    if (int rc = check_part(G, kv_blk_begin, kv_blk_end, head_begin, head_end)) return rc;
+    if (!aligned16(O)) return fail(SPARSP_E_INVALID, "O must be 16-byte aligned");
+    const sparsp::AttnPart part{kv_blk_begin, kv_blk_end, head_begin, head_end,
+                                accumulate ? 1 : 0};
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e =
+        G.bf16 ? sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed,
+                                          capacity_blocks, softmax_scale, part, O, false, lse, s)
+               : sparsp::launch_attn_f32(G, (const float*)Q, sel, keep, slot_of,
+                                         (const float*)K_packed, (const float*)V_packed,
+                                         capacity_blocks, softmax_scale, part, O, lse, s);
+    return hip_status(e, "sparsp_block_sparse_attn_part");
+}
+
+int sparsp_lse_merge(const sparsp_geom* g, int32_t head_begin, int32_t head_end, float* O_acc,
+                     float* lse_acc, const float* O_part, const float* lse_part, void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!O_acc || !lse_acc || !O_part || !lse_part)
+        return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (int rc = check_part(G, 0, G.n, head_begin, head_end)) return rc;
+    if (G.d % 4) return fail(SPARSP_E_UNSUPPORTED, "d = %d must be a multiple of 4", G.d);
+    if (!aligned16(O_acc) || !aligned16(O_part))
+        return fail(SPARSP_E_INVALID, "O_acc and O_part must be 16-byte aligned");
+    if (O_acc == O_part || lse_acc == lse_part)
+        return fail(SPARSP_E_INVALID, "the part may not alias the accumulator");
+    hipError_t e = sparsp::launch_lse_merge(G, head_begin, head_end, O_acc, lse_acc, O_part,
+                                            lse_part, (hipStream_t)stream);
+    return hip_status(e, "sparsp_lse_merge");
+}
+
+int sparsp_chunked_attn(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t keep,
+                        const int32_t* slot_of, const void* K_packed, const void* V_packed,
+                        int64_t capacity_blocks, float softmax_scale, const sparsp_chunk* plan,
+                        int32_t n_chunks, float* O, float* lse, void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!O || !lse || (n_chunks > 0 && !plan)) return fail(SPARSP_E_INVALID, "NULL pointer");
+    if (n_chunks < 0) return fail(SPARSP_E_INVALID, "n_chunks < 0");
+    if (int rc = check_attn(G, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                            softmax_scale))
+        return rc;
+    for (int c = 0; c < n_chunks; ++c)
+        if (int rc = check_part(G, plan[c].kv_blk_begin, plan[c].kv_blk_end, plan[c].head_begin,
+                                plan[c].head_end))
+            return rc;
+    if (!aligned16(O)) return fail(SPARSP_E_INVALID, "O must be 16-byte aligned");
+    hipError_t e = sparsp::run_chunks(G, Q, sel, keep, slot_of, K_packed, V_packed,
+                                      capacity_blocks, softmax_scale, plan, n_chunks, O, lse,
+                                      (hipStream_t)stream);
+    return hip_status(e, "sparsp_chunked_attn");
 }
 
 }  // extern "C"

@@ -137,8 +137,9 @@ __global__ __launch_bounds__(4 * BLK) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict__ sel,
                       const int32_t* __restrict__ slot_of, const uint16_t* __restrict__ Kp,
                       const uint16_t* __restrict__ Vp, void* __restrict__ O,
-                      float* __restrict__ lse, int H, int L, int n, int i0, int nq, int keep,
-                      int64_t capacity, float c2 /* scale * log2(e) */, int remap) {
+                      float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
+                      int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
+                      int h_lo, int n_heads, int acc, int remap) {
     using C = Cfg<D, BLK>;
     // [buffer][K tile | V tile]; reused for the final merge.
     __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][C::TILE];
@@ -151,30 +152,49 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     const int qg = wave % C::NQG, kh = wave / C::NQG;
 
     // Workgroup -> (head, local query block), XCD-contiguous when remap is on.
-    const int G = H * nq;
+    const int G = n_heads * nq;
     int wg = blockIdx.x;
     if (remap) {
         const int xcd = wg & 7, idx = wg >> 3, per = G >> 3, rem = G & 7;
         wg = xcd * per + min(xcd, rem) + idx;
     }
-    const int h = wg / nq, r = wg % nq;
+    const int h = h_lo + wg / nq, r = wg % nq;
     const int qtok = (i0 + r) * BLK + qg * 32 + qi;
     const bool qvalid = qtok < L;
 
-    // Resolve the kept list once: sel -> slot (and partial-block flag).
+    // Resolve the kept list once: sel -> slot (and partial-block flag), keeping
+    // only the usable entries inside [kv_lo, kv_hi), compacted in list order.
+    __shared__ int wave_cnt[C::NW];
+    int nkeep = 0;
     {
-        const int32_t* srow = sel + int64_t(wg) * keep;
+        const int32_t* srow = sel + (int64_t(h) * nq + r) * keep;
         const int32_t* hslot = slot_of + int64_t(h) * n;
         const bool ragged = (L % BLK) != 0;
-        for (int jj = tid; jj < keep; jj += C::THREADS) {
-            const int j = srow[jj];
+        for (int base = 0; base < keep; base += C::THREADS) {
+            const int jj = base + tid;
             int code = -1;
-            if (j >= 0 && j < n) {
-                const int sl = hslot[j];
-                if (sl >= 0 && sl < capacity && sl < (1 << 30))
-                    code = 2 * sl + ((ragged && j == n - 1) ? 1 : 0);
+            if (jj < keep) {
+                const int j = srow[jj];
+                if (j >= kv_lo && j < kv_hi && j >= 0 && j < n) {
+                    const int sl = hslot[j];
+                    if (sl >= 0 && sl < capacity && sl < (1 << 30))
+                        code = 2 * sl + ((ragged && j == n - 1) ? 1 : 0);
+                }
             }
-            codes[jj] = code;
+            const uint64_t bal = __ballot(code >= 0);
+            if (lane == 0) wave_cnt[wave] = __popcll(bal);
+            __syncthreads();
+            int off = nkeep, total = 0;
+#pragma unroll
+            for (int w = 0; w < C::NW; ++w) {
+                off += w < wave ? wave_cnt[w] : 0;
+                total += wave_cnt[w];
+            }
+            const int below = __builtin_amdgcn_mbcnt_hi(
+                uint32_t(bal >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0));
+            if (code >= 0) codes[off + below] = code;
+            nkeep += total;
+            __syncthreads();  // wave_cnt is rewritten by the next round
         }
     }
 
@@ -201,10 +221,12 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             qf[kt] = __builtin_bit_cast(bf16x8, v);
         }
     }
-    __syncthreads();  // codes visible
-    int code = codes[0];
-    issue(code, 0);
-    int next_code = keep > 1 ? codes[1] : -1;
+    // Folding into a running result: nothing to add when no block is kept here.
+    if (acc && nkeep == 0) return;
+    // (the last compaction round ended with a barrier: codes are visible)
+    int code = nkeep > 0 ? codes[0] : -1;
+    if (nkeep > 0) issue(code, 0);
+    int next_code = nkeep > 1 ? codes[1] : -1;
 
     floatx16 oacc[C::DT];
 #pragma unroll
@@ -213,7 +235,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     float l_run = 0.f;        // this lane's partial row sum
     const int last_cnt = L - (L / BLK) * BLK;  // valid keys of a partial last block
 
-    for (int jj = 0; jj < keep; ++jj) {
+    for (int jj = 0; jj < nkeep; ++jj) {
         const int buf = jj & 1;
         const int cur = code;
         // A workgroup barrier does not wait for outstanding vector-memory
@@ -222,10 +244,10 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         // ones in flight) before the barrier publishes the whole tile.
         wait_vmem_all();
         __syncthreads();  // block jj in LDS; everyone is done with block jj-1
-        if (jj + 1 < keep) {
+        if (jj + 1 < nkeep) {
             issue(next_code, buf ^ 1);
             code = next_code;
-            next_code = (jj + 2 < keep) ? codes[jj + 2] : -1;
+            next_code = (jj + 2 < nkeep) ? codes[jj + 2] : -1;
         }
         if (cur < 0) continue;
 
@@ -329,6 +351,27 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     const float inv = live ? 1.0f / l_tot : 0.f;
     const float fa = w_a * inv, fb = w_b * inv;
     const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + qg * 32 + qi;
+    float lse_out = live ? (m + __log2f(l_tot)) * kLn2 : -INFINITY;
+    // Folding into a running result (O, lse, float32): with both log-sum-exps
+    // in log2 units, the stored rows weigh ka and this part kb. Both lanes of
+    // a row pair read the stored lse before the g == 0 lane rewrites it (the
+    // rewrite depends on the value read).
+    float ka = 0.f, kb = 1.f;
+    bool store = true;
+    if (!OUT_BF16 && acc) {
+        store = live;
+        if (live) {
+            const float la2 = lse[orow] * kLog2e;
+            const float lb2 = m + __log2f(l_tot);
+            const float mm = fmaxf(la2, lb2);
+            const float wa = (la2 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(la2 - mm);
+            const float wb = __builtin_amdgcn_exp2f(lb2 - mm);
+            const float t = wa + wb;
+            ka = wa / t;
+            kb = wb / t;
+            lse_out = (mm + __log2f(t)) * kLn2;
+        }
+    }
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt) {
 #pragma unroll
@@ -340,6 +383,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 const int rr = 4 * q4 + u;
                 o4[u] = live ? oacc[dt][rr] * fa + mine[(dt * 16 + rr) * 64 + lane] * fb : 0.f;
             }
+            if (!store) continue;
             if constexpr (OUT_BF16) {
                 uint16_t* op = static_cast<uint16_t*>(O) + orow * D + d0;
                 uint2 w;
@@ -348,30 +392,41 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 *reinterpret_cast<uint2*>(op) = w;
             } else {
                 float* op = static_cast<float*>(O) + orow * D + d0;
+                if (acc) {
+                    const float4 prev = *reinterpret_cast<const float4*>(op);
+                    o4[0] = ka * prev.x + kb * o4[0];
+                    o4[1] = ka * prev.y + kb * o4[1];
+                    o4[2] = ka * prev.z + kb * o4[2];
+                    o4[3] = ka * prev.w + kb * o4[3];
+                }
                 *reinterpret_cast<float4*>(op) = make_float4(o4[0], o4[1], o4[2], o4[3]);
             }
         }
     }
-    if (lse && g == 0) lse[orow] = live ? (m + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (lse && g == 0 && store) lse[orow] = lse_out;
 }
 
 template <int D, int BLK>
 hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int keep,
                         const int32_t* slot_of, const void* Kp, const void* Vp, int64_t cap,
-                        float scale, void* O, bool out_bf16, float* lse, hipStream_t s) {
+                        float scale, const AttnPart& part, void* O, bool out_bf16, float* lse,
+                        hipStream_t s) {
     using C = Cfg<D, BLK>;
-    const int G = g.H * g.nq;
+    const int n_heads = part.h_hi - part.h_lo;
+    const int G = n_heads * g.nq;
     const float c2 = scale * kLog2e;
     const int remap = 1;
     const size_t dyn = size_t(keep) * sizeof(int32_t);
     if (out_bf16)
         attn_bf16_kernel<D, BLK, true><<<G, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
-            g.H, g.L, g.n, g.i0, g.nq, keep, cap, c2, remap);
+            g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
+            part.acc, remap);
     else
         attn_bf16_kernel<D, BLK, false><<<G, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
-            g.H, g.L, g.n, g.i0, g.nq, keep, cap, c2, remap);
+            g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
+            part.acc, remap);
     return hipGetLastError();
 }
 
@@ -379,20 +434,20 @@ hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int ke
 
 hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, int keep,
                             const int32_t* slot_of, const void* Kp, const void* Vp,
-                            int64_t capacity, float scale, void* O, bool out_bf16, float* lse,
-                            hipStream_t s) {
+                            int64_t capacity, float scale, const AttnPart& part, void* O,
+                            bool out_bf16, float* lse, hipStream_t s) {
     (void)hipGetLastError();
     if (g.d == 128 && g.block == 128)
-        return launch_shape<128, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, O,
+        return launch_shape<128, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                                       out_bf16, lse, s);
     if (g.d == 64 && g.block == 64)
-        return launch_shape<64, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, O,
+        return launch_shape<64, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                                     out_bf16, lse, s);
     if (g.d == 128 && g.block == 64)
-        return launch_shape<128, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, O,
+        return launch_shape<128, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                                      out_bf16, lse, s);
     if (g.d == 64 && g.block == 128)
-        return launch_shape<64, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, O,
+        return launch_shape<64, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                                      out_bf16, lse, s);
     return hipErrorInvalidValue;
 }

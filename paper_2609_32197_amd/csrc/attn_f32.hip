@@ -19,12 +19,12 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     const float* __restrict__ Q, const int32_t* __restrict__ sel, const int32_t* __restrict__ slot_of,
     const float* __restrict__ Kp, const float* __restrict__ Vp, float* __restrict__ O,
     float* __restrict__ lse, int L, int n, int d, int block, int i0, int nq, int keep,
-    int64_t capacity, float c2 /* scale * log2(e) */) {
+    int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi, int h_lo, int acc) {
     __shared__ float ks[kKeys][DMAX];
     __shared__ float vs[DMAX][kKeys];
 
     const int wg = blockIdx.x;
-    const int h = wg / nq, r = wg % nq;
+    const int h = h_lo + wg / nq, r = wg % nq;
     const int tid = threadIdx.x;
     const int nthr = blockDim.x;
     const int qtok = (i0 + r) * block + tid;
@@ -38,10 +38,10 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     }
     float m = -INFINITY, l = 0.f;
 
-    const int32_t* srow = sel + int64_t(wg) * keep;
+    const int32_t* srow = sel + (int64_t(h) * nq + r) * keep;
     for (int jj = 0; jj < keep; ++jj) {
         const int j = srow[jj];
-        if (j < 0 || j >= n) continue;
+        if (j < 0 || j >= n || j < kv_lo || j >= kv_hi) continue;
         const int slot = slot_of[int64_t(h) * n + j];
         if (slot < 0 || slot >= capacity) continue;
         const int cnt = min(block, L - j * block);
@@ -88,6 +88,23 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     const bool live = qvalid && l > 0.f;
     const float inv = live ? 1.0f / l : 0.f;
     const int64_t orow = (int64_t(h) * nq + r) * block + tid;
+    if (acc) {
+        // Fold into the stored result through the log-sum-exp (log2 units);
+        // a row with no key in this part leaves it untouched.
+        if (!live) return;
+        const float la2 = lse[orow] * 1.4426950408889634f;
+        const float lb2 = m + log2f(l);
+        const float mm = fmaxf(la2, lb2);
+        const float wa = la2 == -INFINITY ? 0.f : exp2f(la2 - mm);
+        const float wb = exp2f(lb2 - mm);
+        const float t = wa + wb;
+        const float ka = wa / t, kb = wb / t * inv;
+#pragma unroll
+        for (int c = 0; c < DMAX; ++c)
+            if (c < d) O[orow * d + c] = ka * O[orow * d + c] + kb * o[c];
+        lse[orow] = (mm + log2f(t)) * 0.6931471805599453f;
+        return;
+    }
 #pragma unroll
     for (int c = 0; c < DMAX; ++c)
         if (c < d) O[orow * d + c] = o[c] * inv;
@@ -98,17 +115,20 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
 
 hipError_t launch_attn_f32(const Geom& g, const float* Q, const int32_t* sel, int keep,
                            const int32_t* slot_of, const float* Kp, const float* Vp,
-                           int64_t capacity, float scale, float* O, float* lse, hipStream_t s) {
+                           int64_t capacity, float scale, const AttnPart& part, float* O,
+                           float* lse, hipStream_t s) {
     (void)hipGetLastError();
     const int threads = ((g.block + 63) / 64) * 64;
     const float c2 = scale * 1.4426950408889634f;
-    const int G = g.H * g.nq;
+    const int G = (part.h_hi - part.h_lo) * g.nq;
     if (g.d <= 64)
         attn_f32_kernel<64><<<G, threads, 0, s>>>(Q, sel, slot_of, Kp, Vp, O, lse, g.L, g.n, g.d,
-                                                  g.block, g.i0, g.nq, keep, capacity, c2);
+                                                  g.block, g.i0, g.nq, keep, capacity, c2,
+                                                  part.kv_lo, part.kv_hi, part.h_lo, part.acc);
     else
         attn_f32_kernel<128><<<G, threads, 0, s>>>(Q, sel, slot_of, Kp, Vp, O, lse, g.L, g.n,
-                                                   g.d, g.block, g.i0, g.nq, keep, capacity, c2);
+                                                   g.d, g.block, g.i0, g.nq, keep, capacity, c2,
+                                                   part.kv_lo, part.kv_hi, part.h_lo, part.acc);
     return hipGetLastError();
 }
 

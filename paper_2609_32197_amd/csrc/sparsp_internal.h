@@ -37,14 +37,42 @@ hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void*
                                 uint64_t* demand, int32_t* head_off, int32_t* slot_of,
                                 int32_t* gather_blk, void* Kp, void* Vp, hipStream_t s);
 
+// Which part of the attention a launch computes: the heads [h_lo, h_hi) and,
+// of every kept list, only the blocks inside [kv_lo, kv_hi) (one owner's
+// shard). The whole attention is {0, n, 0, H, 0}. With acc set, the float32
+// (O, lse) already hold a running result and the part is folded into it
+// through the log-sum-exp instead of overwriting it; rows without a kept key
+// in the part are left untouched.
+struct AttnPart {
+    int kv_lo, kv_hi, h_lo, h_hi, acc;
+};
+
 hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, int keep,
                             const int32_t* slot_of, const void* Kp, const void* Vp,
-                            int64_t capacity, float scale, void* O, bool out_bf16, float* lse,
-                            hipStream_t s);
+                            int64_t capacity, float scale, const AttnPart& part, void* O,
+                            bool out_bf16, float* lse, hipStream_t s);
 
 hipError_t launch_attn_f32(const Geom& g, const float* Q, const int32_t* sel, int keep,
                            const int32_t* slot_of, const float* Kp, const float* Vp,
-                           int64_t capacity, float scale, float* O, float* lse, hipStream_t s);
+                           int64_t capacity, float scale, const AttnPart& part, float* O,
+                           float* lse, hipStream_t s);
+
+hipError_t launch_lse_merge(const Geom& g, int h_lo, int h_hi, float* O_acc, float* lse_acc,
+                            const float* O_part, const float* lse_part, hipStream_t s);
+
+hipError_t launch_fill_identity(float* O, float* lse, int64_t rows, int d, hipStream_t s);
+
+// Host: the chunk schedule of rank `rank` (count of chunks written, or minus
+// the count needed when it exceeds max_chunks). demand is host memory [H, W].
+int plan_chunks(const Geom& g, const uint64_t* demand, int ranks, int rank, int heads_per_chunk,
+                int tail_heads_per_chunk, sparsp_chunk* out, int max_chunks);
+
+// Host: runs a validated plan on stream s (one attention launch per chunk,
+// folding into (O, lse)).
+hipError_t run_chunks(const Geom& g, const void* Q, const int32_t* sel, int keep,
+                      const int32_t* slot_of, const void* Kp, const void* Vp, int64_t capacity,
+                      float scale, const sparsp_chunk* plan, int n_chunks, float* O, float* lse,
+                      hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // device helpers

@@ -44,8 +44,15 @@ def test_library_exports_every_declared_symbol(lib):
         assert hasattr(lib, name), name
 
 
+def test_header_declares_the_shard_by_shard_calls():
+    names = declared_functions()
+    for want in ("sparsp_chunk_plan", "sparsp_block_sparse_attn_part", "sparsp_lse_merge",
+                 "sparsp_chunked_attn"):
+        assert want in names
+
+
 def test_version(lib):
-    assert lib.sparsp_version() == 100
+    assert lib.sparsp_version() == 200
 
 
 def geom(H=2, L=1024, d=128, block=128, i0=0, i1=8, dtype=sp.BF16):
@@ -136,3 +143,67 @@ def test_binding_rejects_host_tensors():
 def test_binding_reports_status_names(lib):
     e = sp.SparspError(-4, "capacity_blocks too small")
     assert e.status == "SPARSP_E_CAPACITY" and "capacity" in str(e)
+
+
+# ---------------------------------------------------------------------------
+# the chunk schedule is host code: it runs here, against the oracle
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(8))
+def test_chunk_plan_matches_the_oracle(lib, seed):
+    import numpy as np
+    import oracle as orc
+    rng = np.random.default_rng(100 + seed)
+    H = int(rng.integers(1, 12))
+    block = 16
+    n = int(rng.integers(2, 150))
+    L = n * block - int(rng.integers(0, block))
+    ranks = int(rng.integers(1, min(n, 9) + 1))
+    rank = int(rng.integers(0, ranks))
+    hpc, tail = int(rng.integers(1, 6)), int(rng.integers(1, 4))
+    demand = rng.random((H, n)) < rng.uniform(0.05, 0.9)
+    g = sp.Geometry(H, L, 64, block, 0, 1, sp.F32)
+    got = [c.astuple() for c in sp.sparsp_chunk_plan(g, orc.mask_to_words(demand), ranks, rank,
+                                                     hpc, tail)]
+    assert got == orc.chunk_plan(demand, ranks, rank, hpc, tail)
+
+
+def test_chunk_plan_rejected(lib):
+    import numpy as np
+    g = geom(H=4, L=1024, block=128, i0=0, i1=8)  # n = 8
+    dem = np.zeros((4, 1), dtype=np.uint64)
+    arr = (sp.Chunk * 64)()
+    call = lambda ranks, rank, a, b, cap=64: lib.sparsp_chunk_plan(
+        ctypes.byref(g), dem.ctypes.data, ranks, rank, a, b, arr, cap)
+    assert call(0, 0, 1, 1) == E_INVALID
+    assert call(9, 0, 1, 1) == E_INVALID  # more ranks than blocks
+    assert call(4, 4, 1, 1) == E_INVALID
+    assert call(4, -1, 1, 1) == E_INVALID
+    assert call(4, 0, 0, 1) == E_INVALID
+    assert call(4, 0, 1, 0) == E_INVALID
+    assert call(4, 0, 1, 1, cap=12) == E_CAPACITY  # needs 1 + 3 * 4 = 13
+    assert b"13" in lib.sparsp_last_error()
+    assert call(4, 0, 1, 1, cap=13) == 13
+    assert call(1, 0, 1, 1) == 1
+    assert lib.sparsp_chunk_plan(ctypes.byref(g), None, 4, 0, 1, 1, arr, 64) == E_INVALID
+
+
+def test_part_and_merge_rejected(lib):
+    g = geom()  # H = 2, n = 8
+    part = lambda lo, hi, h0, h1, lse=P: lib.sparsp_block_sparse_attn_part(
+        ctypes.byref(g), P, P, 2, P, P, P, 16, 0.125, lo, hi, h0, h1, P, lse, 0, None)
+    assert part(0, 9, 0, 2) == E_INVALID
+    assert part(-1, 4, 0, 2) == E_INVALID
+    assert part(5, 4, 0, 2) == E_INVALID
+    assert part(0, 8, 1, 1) == E_INVALID
+    assert part(0, 8, 0, 3) == E_INVALID
+    assert part(0, 8, 0, 2, lse=None) == E_INVALID  # lse is required
+    merge = lambda h0, h1, a=P, b=P + 4096: lib.sparsp_lse_merge(
+        ctypes.byref(g), h0, h1, a, a + 8192, b, b + 8192, None)
+    assert merge(0, 3) == E_INVALID
+    assert merge(1, 1) == E_INVALID
+    assert merge(0, 2, b=P) == E_INVALID  # part aliases the accumulator
+    assert merge(0, 2, a=P + 4) == E_INVALID  # misaligned
+    bad = (sp.Chunk * 1)(sp.Chunk(0, 0, 9, 0, 2, 0))
+    assert lib.sparsp_chunked_attn(ctypes.byref(g), P, P, 2, P, P, P, 16, 0.125, bad, 1, P, P,
+                                   None) == E_INVALID
