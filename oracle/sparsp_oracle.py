@@ -17,6 +17,9 @@ The computation follows the paper (arXiv 2609.32197):
 * Section 5.2: demand is kept per head (not unioned across heads) and blocks
   are packed row-major, each head a contiguous range, so that offsets can be
   derived locally on both ends.
+* Section 4.3, Eq. 4: the interval-periodic layout gives spatial interval
+  floor(G s / B) of every frame to the same rank, realised as a block
+  permutation of the sequence and its inverse;
 * Section 2.3 and Section 7: a rank attends to the KV shards of the owners
   one at a time and combines the partial results with the online softmax;
   Section 7.1 keeps the local shard whole and cuts the last remote shard into
@@ -36,6 +39,11 @@ Readings taken where the paper is silent:
   what Eq. 3 counts;
 * the packed K buffer keeps each block as [block, d]; the packed V buffer
   stores each block transposed, [d, block]; token rows past L are zero;
+* placement: a block's frame position is that of its first token, so block j
+  goes to rank floor(G (j b mod F) / F) for F tokens per frame (Eq. 4 exactly
+  when F is a multiple of b); a ragged last block stays last and belongs to
+  the last rank; the placed order lists each rank's blocks in logical order,
+  rank after rank;
 * a chunk is (owner shard, run of consecutive heads); shards are taken in
   ring order from the local one (r, r+1, ..., r+R-1 mod R); remote shards are
   cut into chunks of a given number of heads, the last remote shard into
@@ -82,6 +90,13 @@ __all__ = [
     "lse_merge",
     "chunk_plan",
     "chunked_attention",
+    "periodic_owner",
+    "contiguous_owner",
+    "placement_permutation",
+    "inverse_permutation",
+    "permute_blocks",
+    "rank_demand",
+    "remote_blocks",
 ]
 
 
@@ -496,3 +511,80 @@ def chunked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, mask: np.ndar
         O[~keep_rows] = np.nan
         LSE[~keep_rows] = np.nan
     return O, LSE
+
+
+# ---------------------------------------------------------------------------
+# Section 4.3, Eq. 4: dependency-aware (interval-periodic) placement
+# ---------------------------------------------------------------------------
+
+def periodic_owner(L: int, block: int, frame_tokens: int, ranks: int) -> np.ndarray:
+    """Owner of every logical block under Eq. 4: floor(G s / B).
+
+    With F = frame_tokens and s / B read as the spatial offset of the block's
+    first token inside its frame over the frame size, block j goes to
+    floor(G ((j b) mod F) / F). A ragged last block belongs to the last rank.
+    """
+    n = num_blocks(L, block)
+    j = np.arange(n, dtype=np.int64)
+    owner = (ranks * ((j * block) % frame_tokens)) // frame_tokens
+    if L % block:
+        owner[n - 1] = ranks - 1
+    return owner.astype(np.int64)
+
+
+def contiguous_owner(n: int, ranks: int) -> np.ndarray:
+    """Owner of every block when rank p holds [floor(p n / R), floor((p+1) n / R))."""
+    owner = np.empty(n, dtype=np.int64)
+    for p in range(ranks):
+        lo, hi = local_range(n, ranks, p)
+        owner[lo:hi] = p
+    return owner
+
+
+def placement_permutation(owner: np.ndarray, ranks: int) -> tuple:
+    """The placed order: rank 0's blocks in logical order, then rank 1's, ...
+
+    Returns (perm, rank_begin): perm[k] is the logical block at placed
+    position k, and rank p holds the placed positions [rank_begin[p],
+    rank_begin[p+1]).
+    """
+    perm = np.concatenate([np.nonzero(owner == p)[0] for p in range(ranks)]).astype(np.int64)
+    counts = np.array([(owner == p).sum() for p in range(ranks)], dtype=np.int64)
+    rank_begin = np.concatenate([[0], np.cumsum(counts)])
+    return perm, rank_begin
+
+
+def inverse_permutation(perm: np.ndarray) -> np.ndarray:
+    """inv[perm[k]] = k."""
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(perm.shape[0], dtype=perm.dtype)
+    return inv
+
+
+def permute_blocks(X: np.ndarray, perm: np.ndarray, L: int, block: int) -> np.ndarray:
+    """Token tensor [H, L, d] in placed order: placed block k holds logical block perm[k].
+
+    Block membership is unchanged (whole blocks move); the ragged last block,
+    if any, is the last logical block and stays last.
+    """
+    Y = np.empty_like(X)
+    for k, j in enumerate(perm):
+        c = min(block, L - int(j) * block)
+        assert c == min(block, L - k * block), "only the last block may be ragged"
+        Y[:, k * block:k * block + c] = X[:, int(j) * block:int(j) * block + c]
+    return Y
+
+
+def rank_demand(mask_all: np.ndarray, owner: np.ndarray, rank: int) -> np.ndarray:
+    """Eq. 2 over every owner: D_r[h, j] = exists i with owner(i) = r and M[h, i, j].
+
+    mask_all: bool [H, n, n] over every query block (logical indices).
+    Returns bool [H, n]; D_{r,h,p} is its restriction to owner(j) = p.
+    """
+    rows = owner == rank
+    return mask_all[:, rows, :].any(axis=1)
+
+
+def remote_blocks(demand: np.ndarray, owner: np.ndarray, rank: int) -> int:
+    """sum over h and p != r of |D_{r,h,p}|: Eq. 3's block count (times 2 b d w for bytes)."""
+    return int((demand & (owner[None, :] != rank)).sum())
