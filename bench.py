@@ -234,6 +234,62 @@ def measure_chunked(sp, g, wl, Q, bufs, packed, stream, a):
     }
 
 
+def measure_placement(sp, g, wl, Q, K, V, bufs, packed, stream, ranks_list=(4, 8)):
+    """Dependency-aware placement (Section 4.3, Eq. 4) against contiguous slices.
+
+    For each R, every rank r runs scores, top-k and demand over its own query
+    blocks, with the tensors in logical order (contiguous slices) or in Eq. 4's
+    placed order; the sums over ranks of the demanded blocks (sum of U_h) and
+    of Eq. 3's remote blocks are reported, with the largest V_r in bytes. The
+    block permutation kernel is timed on Q.
+    """
+    import torch
+    T, Hy, W = wl.latent
+    F = Hy * W
+    b, d, w = wl.block, wl.d, wl.bytes_per_elem
+    Qp, Kp = torch.empty_like(Q), torch.empty_like(K)
+    res = {"frame_tokens": F}
+
+    def rank_stats(Qx, Kx, begin):
+        demanded, remote, worst = 0, 0, 0
+        for r in range(len(begin) - 1):
+            gr = sp.Geometry(wl.H, wl.L, wl.d, wl.block, int(begin[r]), int(begin[r + 1]), g.dtype)
+            _, _, sc = sp.sparsp_block_scores(gr, Qx, Kx, stream=stream)
+            m, _ = sp.sparsp_topk_mask(gr, sc, wl.keep, wl.global_blocks, stream=stream)
+            sp.sparsp_demand_union_gather(gr, m, Kx, Kx, wl.H * wl.n, out=packed, stream=stream)
+            rem, tot = sp.sparsp_remote_demand(gr, packed["demand"])
+            demanded += tot
+            remote += rem
+            worst = max(worst, rem)
+        return {"demanded_blocks": demanded, "remote_blocks": remote,
+                "max_rank_remote_blocks": worst, "max_rank_V_bytes": 2 * b * d * w * worst,
+                "total_V_bytes": 2 * b * d * w * remote}
+
+    for R in ranks_list:
+        if R > wl.n:
+            continue
+        contiguous = [(p * wl.n) // R for p in range(R + 1)]
+        perm, begin = sp.sparsp_periodic_placement(wl.L, b, F, R)
+        pd = torch.from_numpy(perm).cuda()
+        sp.sparsp_permute_blocks(g, pd, Q, Qp, stream=stream)
+        sp.sparsp_permute_blocks(g, pd, K, Kp, stream=stream)
+        c = rank_stats(Q, K, contiguous)
+        pr = rank_stats(Qp, Kp, begin)
+        res[f"R{R}"] = {
+            "contiguous": c, "periodic": pr,
+            "remote_reduction": 1.0 - pr["remote_blocks"] / max(1, c["remote_blocks"]),
+            "demand_reduction": 1.0 - pr["demanded_blocks"] / max(1, c["demanded_blocks"]),
+            "periodic_rank_blocks": [int(begin[p + 1] - begin[p]) for p in range(R)],
+        }
+        if "permute" not in res:
+            ms = time_calls(lambda: sp.sparsp_permute_blocks(g, pd, Q, Qp, stream=stream), 5, stream)
+            nbytes = 2 * wl.H * wl.L * wl.d * w
+            res["permute"] = {"ms": ms, "bytes": nbytes, "GBps": nbytes / (ms * 1e-3) / 1e9,
+                              "frac_of_hbm_peak": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS}
+    del Qp, Kp
+    return res
+
+
 def main(argv=None) -> int:
     a = parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -380,6 +436,14 @@ def main(argv=None) -> int:
         c = rec["chunked_attention"]
         log(f"[bench] shard-by-shard: {c['chunks']} chunks {c['chunked_ms']:.3f} ms vs "
             f"{c['unchunked_f32_out_ms']:.3f} ms unchunked; merge {c['merge']['GBps']:.0f} GB/s")
+    if not a.no_extensions and wl.ranks > 1 and not wl.global_blocks:
+        # (reuses the step's packed buffers: runs last)
+        rec["placement"] = measure_placement(sp, g, wl, Q, K, V, bufs, packed, stream)
+        for key, val in rec["placement"].items():
+            if key.startswith("R"):
+                log(f"[bench] placement {key}: remote blocks contiguous "
+                    f"{val['contiguous']['remote_blocks']} -> periodic {val['periodic']['remote_blocks']}"
+                    f" ({100 * val['remote_reduction']:.1f}% less)")
     log(f"[bench] {wl.name}: {ms_per_step:.3f} ms/layer, attention {stage_ms['block_sparse_attn']:.3f} ms "
         f"= {attn_tflops:.0f} TFLOP/s ({100 * attn_tflops / peak:.1f}% of peak), stages {stage_ms}")
     if not a.no_cpu_baseline:

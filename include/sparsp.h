@@ -232,6 +232,47 @@ int sparsp_chunked_attn(const sparsp_geom* g, const void* Q, const int32_t* sel,
                         int64_t capacity_blocks, float softmax_scale, const sparsp_chunk* plan,
                         int32_t n_chunks, float* O, float* lse, void* stream);
 
+/*
+ * Dependency-aware placement (Section 4.3, Eq. 4): spatial interval
+ * floor(G s / B) of every frame goes to the same rank. Block j (tokens in
+ * frame-major raster order, F = frame_tokens per frame) goes to rank
+ * floor(ranks * ((j * block) mod F) / F), which is Eq. 4 when F is a multiple
+ * of block; a ragged last block stays last and belongs to the last rank. The
+ * placed order lists rank 0's blocks in logical order, then rank 1's, ...
+ *
+ * Outputs (HOST): perm [n] with perm[k] = the logical block at placed position
+ * k, and rank_begin [ranks + 1]: rank p holds placed blocks [rank_begin[p],
+ * rank_begin[p+1]) (use them as q_blk_begin / q_blk_end of that rank's geometry
+ * over placed tensors). Errors: non-positive sizes, ranks > n, NULL pointers.
+ * Pure host code.
+ */
+int sparsp_periodic_placement(int32_t L, int32_t block, int32_t frame_tokens, int32_t ranks,
+                              int32_t* perm, int32_t* rank_begin);
+
+/*
+ * Moves whole token blocks of X [H, L, d] (geom.dtype) into Y: Y block k =
+ * X block perm[k] (inverse == 0, into placed order) or Y block perm[k] =
+ * X block k (inverse != 0, back to logical order). perm: DEVICE int32 [n], a
+ * permutation of [0, n) that keeps a ragged last block last (as
+ * sparsp_periodic_placement returns); an entry outside [0, n) leaves its
+ * destination block untouched, and blocks of unequal valid rows copy the
+ * smaller count, so a malformed perm cannot make the kernel leave the tensors.
+ * X and Y must not overlap and must be 16-byte aligned.
+ */
+int sparsp_permute_blocks(const sparsp_geom* g, const int32_t* perm, const void* X, void* Y,
+                          int32_t inverse, void* stream);
+
+/*
+ * Eq. 3's block count for the rank whose own blocks are the geometry's
+ * [q_blk_begin, q_blk_end) (in whatever layout, placed or contiguous, the
+ * tensors are in): *remote = sum over heads of the demanded blocks outside that
+ * range (sum_{p != r} |D_{r,h,p}|; times 2 * block * d * w it is V_r), and
+ * *demanded = all demanded blocks (sum of U_h). demand: HOST uint64 [H, W] as
+ * sparsp_demand_union_gather writes it. Pure host code.
+ */
+int sparsp_remote_demand(const sparsp_geom* g, const uint64_t* demand, int64_t* remote,
+                         int64_t* demanded);
+
 /* Message of the calling thread's most recent error ("" if none). */
 const char* sparsp_last_error(void);
 

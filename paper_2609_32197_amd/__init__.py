@@ -18,6 +18,12 @@ Shard-by-shard attention (Section 2.3, Section 7):
     sparsp_lse_merge               online-softmax merge of two partial results
     sparsp_chunked_attn            a whole schedule, attended and merged
 
+Dependency-aware placement (Section 4.3, Eq. 4):
+
+    sparsp_periodic_placement      placed order of the blocks per rank (host)
+    sparsp_permute_blocks          token blocks into placed order and back
+    sparsp_remote_demand           Eq. 3's remote block count of a rank (host)
+
 Short aliases without the prefix are provided as well.
 """
 
@@ -53,6 +59,12 @@ __all__ = [
     "block_sparse_attn_part",
     "lse_merge",
     "chunked_attn",
+    "sparsp_periodic_placement",
+    "sparsp_permute_blocks",
+    "sparsp_remote_demand",
+    "periodic_placement",
+    "permute_blocks",
+    "remote_demand",
     "F32",
     "BF16",
     "STATUS",
@@ -142,6 +154,10 @@ _SIGNATURES = {
     "sparsp_lse_merge": [ctypes.POINTER(_Geom), _I32, _I32, _VP, _VP, _VP, _VP, _VP],
     "sparsp_chunked_attn": [ctypes.POINTER(_Geom), _VP, _VP, _I32, _VP, _VP, _VP, ctypes.c_int64,
                             ctypes.c_float, ctypes.POINTER(Chunk), _I32, _VP, _VP, _VP],
+    "sparsp_periodic_placement": [_I32, _I32, _I32, _I32, _VP, _VP],
+    "sparsp_permute_blocks": [ctypes.POINTER(_Geom), _VP, _VP, _VP, _I32, _VP],
+    "sparsp_remote_demand": [ctypes.POINTER(_Geom), _VP, ctypes.POINTER(ctypes.c_int64),
+                             ctypes.POINTER(ctypes.c_int64)],
 }
 
 
@@ -446,6 +462,49 @@ def sparsp_chunked_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed, pla
     return o, ls
 
 
+# ---------------------------------------------------------------------------
+# dependency-aware placement
+# ---------------------------------------------------------------------------
+
+def sparsp_periodic_placement(L: int, block: int, frame_tokens: int, ranks: int) -> tuple:
+    """Eq. 4's placed order (host). Returns (perm int32 [n], rank_begin int32 [ranks+1]) as numpy."""
+    import numpy as np
+    n = -(-int(L) // int(block))
+    perm = np.empty(n, dtype=np.int32)
+    begin = np.empty(int(ranks) + 1, dtype=np.int32)
+    _check(load_library().sparsp_periodic_placement(int(L), int(block), int(frame_tokens),
+                                                    int(ranks), perm.ctypes.data,
+                                                    begin.ctypes.data))
+    return perm, begin
+
+
+def sparsp_permute_blocks(geom: Geometry, perm, X, Y=None, inverse: bool = False, stream=None):
+    """Token blocks of X [H, L, d] into placed order (or back, with inverse). perm: int32 [n] on the GPU."""
+    torch = _torch()
+    g = geom
+    et = _elem_dtype(g)
+    y = Y if Y is not None else torch.empty_like(X)
+    args = (_dev(perm, "perm", torch.int32, (g.n,)), _dev(X, "X", et, (g.H, g.L, g.d)),
+            _dev(y, "Y", et, (g.H, g.L, g.d)), int(bool(inverse)))
+    gs = g.c_struct()
+    _check(load_library().sparsp_permute_blocks(ctypes.byref(gs), *args, _stream(stream, X.device)))
+    return y
+
+
+def sparsp_remote_demand(geom: Geometry, demand) -> tuple:
+    """(remote blocks outside [i0, i1), all demanded blocks) from demand [H, W] (any device)."""
+    import numpy as np
+    g = geom
+    if hasattr(demand, "detach"):
+        demand = demand.detach().cpu().numpy()
+    dem = np.ascontiguousarray(np.asarray(demand).view(np.uint64).reshape(g.H, g.W))
+    rem, alld = ctypes.c_int64(), ctypes.c_int64()
+    gs = g.c_struct()
+    _check(load_library().sparsp_remote_demand(ctypes.byref(gs), dem.ctypes.data,
+                                               ctypes.byref(rem), ctypes.byref(alld)))
+    return rem.value, alld.value
+
+
 block_scores = sparsp_block_scores
 topk_mask = sparsp_topk_mask
 demand_union_gather = sparsp_demand_union_gather
@@ -454,3 +513,6 @@ chunk_plan = sparsp_chunk_plan
 block_sparse_attn_part = sparsp_block_sparse_attn_part
 lse_merge = sparsp_lse_merge
 chunked_attn = sparsp_chunked_attn
+periodic_placement = sparsp_periodic_placement
+permute_blocks = sparsp_permute_blocks
+remote_demand = sparsp_remote_demand

@@ -302,4 +302,39 @@ int sparsp_chunked_attn(const sparsp_geom* g, const void* Q, const int32_t* sel,
     return hip_status(e, "sparsp_chunked_attn");
 }
 
+int sparsp_periodic_placement(int32_t L, int32_t block, int32_t frame_tokens, int32_t ranks,
+                              int32_t* perm, int32_t* rank_begin) {
+    if (!perm || !rank_begin) return fail(SPARSP_E_INVALID, "NULL pointer");
+    if (L <= 0 || block <= 0 || frame_tokens <= 0 || ranks <= 0)
+        return fail(SPARSP_E_INVALID, "L, block, frame_tokens and ranks must be positive");
+    const int64_t n = (int64_t(L) + block - 1) / block;
+    if (n > sparsp::kMaxBlocks)
+        return fail(SPARSP_E_UNSUPPORTED, "n = %lld blocks exceeds %d", (long long)n,
+                    sparsp::kMaxBlocks);
+    if (ranks > n) return fail(SPARSP_E_INVALID, "ranks = %d exceeds n = %lld", ranks, (long long)n);
+    sparsp::periodic_placement(L, block, frame_tokens, ranks, perm, rank_begin);
+    return ok();
+}
+
+int sparsp_permute_blocks(const sparsp_geom* g, const int32_t* perm, const void* X, void* Y,
+                          int32_t inverse, void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!perm || !X || !Y) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (X == Y) return fail(SPARSP_E_INVALID, "X and Y must not overlap");
+    if (!aligned16(X) || !aligned16(Y))
+        return fail(SPARSP_E_INVALID, "X and Y must be 16-byte aligned");
+    hipError_t e = sparsp::launch_permute(G, perm, X, Y, inverse != 0, (hipStream_t)stream);
+    return hip_status(e, "sparsp_permute_blocks");
+}
+
+int sparsp_remote_demand(const sparsp_geom* g, const uint64_t* demand, int64_t* remote,
+                         int64_t* demanded) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!demand || !remote || !demanded) return fail(SPARSP_E_INVALID, "NULL pointer");
+    sparsp::remote_demand(G, demand, remote, demanded);
+    return ok();
+}
+
 }  // extern "C"

@@ -67,6 +67,16 @@ hipError_t launch_fill_identity(float* O, float* lse, int64_t rows, int d, hipSt
 int plan_chunks(const Geom& g, const uint64_t* demand, int ranks, int rank, int heads_per_chunk,
                 int tail_heads_per_chunk, sparsp_chunk* out, int max_chunks);
 
+// Host: Eq. 4's placed order of the blocks (perm [n], rank_begin [ranks+1]).
+void periodic_placement(int L, int block, int frame_tokens, int ranks, int32_t* perm,
+                        int32_t* rank_begin);
+
+hipError_t launch_permute(const Geom& g, const int32_t* perm, const void* X, void* Y, bool inverse,
+                          hipStream_t s);
+
+// Host: demanded blocks outside [i0, i1) and in total, over all heads.
+void remote_demand(const Geom& g, const uint64_t* demand, int64_t* remote, int64_t* demanded);
+
 // Host: runs a validated plan on stream s (one attention launch per chunk,
 // folding into (O, lse)).
 hipError_t run_chunks(const Geom& g, const void* Q, const int32_t* sel, int keep,

@@ -207,3 +207,59 @@ def test_part_and_merge_rejected(lib):
     bad = (sp.Chunk * 1)(sp.Chunk(0, 0, 9, 0, 2, 0))
     assert lib.sparsp_chunked_attn(ctypes.byref(g), P, P, 2, P, P, P, 16, 0.125, bad, 1, P, P,
                                    None) == E_INVALID
+
+
+# ---------------------------------------------------------------------------
+# placement and the Eq. 3 count are host code: they run here, against the oracle
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", range(8))
+def test_periodic_placement_matches_the_oracle(lib, seed):
+    import numpy as np
+    import oracle as orc
+    rng = np.random.default_rng(200 + seed)
+    block = int(rng.choice([8, 16, 64, 128]))
+    F = int(rng.integers(block // 2 + 1, 40 * block))
+    L = int(rng.integers(2 * block, 3000 * 8))
+    n = -(-L // block)
+    if n > 4096:
+        L = 4096 * block
+        n = 4096
+    ranks = int(rng.integers(1, min(n, 9) + 1))
+    perm, begin = sp.sparsp_periodic_placement(L, block, F, ranks)
+    operm, obegin = orc.placement_permutation(orc.periodic_owner(L, block, F, ranks), ranks)
+    assert perm.tolist() == operm.tolist() and begin.tolist() == obegin.tolist()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_remote_demand_matches_the_oracle(lib, seed):
+    import numpy as np
+    import oracle as orc
+    rng = np.random.default_rng(300 + seed)
+    H, n = int(rng.integers(1, 9)), int(rng.integers(2, 300))
+    ranks = int(rng.integers(1, min(n, 8) + 1))
+    r = int(rng.integers(0, ranks))
+    lo, hi = orc.local_range(n, ranks, r)
+    demand = rng.random((H, n)) < 0.3
+    g = sp.Geometry(H, n * 16, 64, 16, lo, hi, sp.F32)
+    remote, total = sp.sparsp_remote_demand(g, orc.mask_to_words(demand))
+    assert remote == orc.remote_blocks(demand, orc.contiguous_owner(n, ranks), r)
+    assert total == int(demand.sum())
+
+
+def test_placement_and_permute_rejected(lib):
+    import numpy as np
+    perm = np.zeros(64, dtype=np.int32)
+    begin = np.zeros(9, dtype=np.int32)
+    call = lambda L, b, F, R: lib.sparsp_periodic_placement(L, b, F, R, perm.ctypes.data,
+                                                           begin.ctypes.data)
+    assert call(0, 8, 64, 2) == E_INVALID
+    assert call(64, 0, 64, 2) == E_INVALID
+    assert call(64, 8, 0, 2) == E_INVALID
+    assert call(64, 8, 64, 0) == E_INVALID
+    assert call(64, 8, 64, 9) == E_INVALID  # more ranks than blocks
+    assert lib.sparsp_periodic_placement(64, 8, 64, 2, None, begin.ctypes.data) == E_INVALID
+    g = geom()
+    assert lib.sparsp_permute_blocks(ctypes.byref(g), P, P, P, 0, None) == E_INVALID  # X == Y
+    assert lib.sparsp_permute_blocks(ctypes.byref(g), P, P, P + 8, 0, None) == E_INVALID
+    assert lib.sparsp_permute_blocks(ctypes.byref(g), None, P, P + 4096, 0, None) == E_INVALID

@@ -61,7 +61,7 @@ class Workload:
     keep_abs: Optional[int]
     ranks: int
     rank: int
-    feature: str  # "iid" or "sinusoid"
+    feature: str  # "iid", "sinusoid" or "sinusoid-spatial"
 
     # ---- derived geometry -------------------------------------------------
     @property
@@ -152,6 +152,11 @@ CONFIGS = {
     "hunyuan-layer-dense": _cfg(name="hunyuan-layer-dense", config_id=4, H=24, d=128, block=128,
                                 latent=(33, 45, 80), dtype="bf16", keep_pct=100),
 }
+# The wan-style layer with a frame-independent feature (no temporal frequency):
+# attention then depends on the in-frame position alone, the multi-diagonal
+# pattern of Section 4.3. Used only to study placement.
+CONFIGS["wan-share-multidiag"] = dataclasses.replace(
+    CONFIGS["wan-share"], name="wan-share-multidiag", config_id=6, feature="sinusoid-spatial")
 # Density / text-token sweep: 13x30x45 video + 226 text tokens, rank 0 of 2.
 for _pct in (5, 10, 25, 50, 100):
     CONFIGS[f"text-sweep-{_pct}"] = _cfg(
@@ -199,9 +204,14 @@ def _head_streams(wl: Workload, seed: int):
 
 
 def _sinusoid_feature(wl: Workload, ss: np.random.SeedSequence) -> np.ndarray:
-    """f[tok, c] = sqrt(2) cos(2 pi (nu_t t/T + nu_y y/Hy + nu_x x/W) + phi) on video tokens."""
+    """f[tok, c] = sqrt(2) cos(2 pi (nu_t t/T + nu_y y/Hy + nu_x x/W) + phi) on video tokens.
+
+    With the "sinusoid-spatial" feature nu_t is 0: the same in every frame.
+    """
     rng = np.random.Generator(np.random.PCG64(ss))
     nu = rng.uniform(0.0, 2.0, size=(wl.d, 3))
+    if wl.feature == "sinusoid-spatial":
+        nu[:, 0] = 0.0
     phi = rng.uniform(0.0, 2.0 * np.pi, size=wl.d)
     T, Hy, W = wl.latent
     t = np.arange(T, dtype=np.float64)[:, None, None] / T
@@ -224,7 +234,7 @@ def _finish(x64: np.ndarray, dtype: str) -> np.ndarray:
 def _one_head(wl: Workload, streams, h: int):
     out = []
     feat = None
-    if wl.feature == "sinusoid":
+    if wl.feature in ("sinusoid", "sinusoid-spatial"):
         feat = _sinusoid_feature(wl, streams[_FEAT][h])
     for t in (_Q, _K, _V):
         rng = np.random.Generator(np.random.PCG64(streams[t][h]))
