@@ -17,6 +17,9 @@ The computation follows the paper (arXiv 2609.32197):
 * Section 5.2: demand is kept per head (not unioned across heads) and blocks
   are packed row-major, each head a contiguous range, so that offsets can be
   derived locally on both ends.
+* Section 8.1: the evaluation's selection rule (CDF mode) keeps, for each
+  query, the highest-scoring key blocks until their cumulative attention mass
+  reaches a threshold tau;
 * Section 4.3, Eq. 4: the interval-periodic layout gives spatial interval
   floor(G s / B) of every frame to the same rank, realised as a block
   permutation of the sequence and its inverse;
@@ -44,6 +47,10 @@ Readings taken where the paper is silent:
   when F is a multiple of b); a ragged last block stays last and belongs to
   the last rank; the placed order lists each rank's blocks in logical order,
   rank after rank;
+* CDF mode per query block: the softmax of the row's float32 block scores over
+  all n blocks; blocks ordered by (score descending, index ascending); the
+  shortest prefix of that order whose mass reaches tau is kept, then the
+  diagonal and global blocks are added; tau in (0, 1];
 * a chunk is (owner shard, run of consecutive heads); shards are taken in
   ring order from the local one (r, r+1, ..., r+R-1 mod R); remote shards are
   cut into chunks of a given number of heads, the last remote shard into
@@ -97,6 +104,8 @@ __all__ = [
     "permute_blocks",
     "rank_demand",
     "remote_blocks",
+    "cdf_order_and_mass",
+    "select_cdf",
 ]
 
 
@@ -588,3 +597,58 @@ def rank_demand(mask_all: np.ndarray, owner: np.ndarray, rank: int) -> np.ndarra
 def remote_blocks(demand: np.ndarray, owner: np.ndarray, rank: int) -> int:
     """sum over h and p != r of |D_{r,h,p}|: Eq. 3's block count (times 2 b d w for bytes)."""
     return int((demand & (owner[None, :] != rank)).sum())
+
+
+# ---------------------------------------------------------------------------
+# Section 8.1: CDF-mode selection (cumulative attention mass up to tau)
+# ---------------------------------------------------------------------------
+
+def cdf_order_and_mass(score_row: np.ndarray) -> tuple:
+    """The CDF order of one row and the cumulative softmax mass along it.
+
+    score_row: float32 [n]. Returns (order int64 [n]: blocks by score
+    descending, then index ascending; mass float64 [n]: mass[k] is the softmax
+    mass of the first k+1 blocks of that order, mass[n-1] = 1).
+    """
+    s = np.asarray(score_row)
+    if s.dtype != np.float32:
+        raise TypeError("scores must be float32")
+    if np.isnan(s).any():
+        raise ValueError("NaN block score")
+    s64 = s.astype(np.float64)
+    order = np.lexsort((np.arange(s.shape[0]), -s64))
+    p = np.exp(s64 - s64.max())
+    mass = np.cumsum(p[order]) / p.sum()
+    mass[-1] = 1.0
+    return order.astype(np.int64), mass
+
+
+def select_cdf(scores: np.ndarray, tau: float, i0: int, global_blocks: Sequence[int] = ()) -> tuple:
+    """CDF-mode block mask: the shortest prefix of the CDF order with mass >= tau, plus F_i.
+
+    scores: float32 [H, nq, n]; row r is global query block i0 + r. Returns
+    (mask bool [H, nq, n], sel int32 [H, nq, n]: each row's kept blocks
+    ascending then -1, counts int32 [H, nq]).
+    """
+    if not 0.0 < tau <= 1.0:
+        raise ValueError("tau must be in (0, 1]")
+    s = np.asarray(scores)
+    H, nq, n = s.shape
+    G = sorted({int(g) for g in global_blocks})
+    if any(g < 0 or g >= n for g in G):
+        raise ValueError("global block out of range")
+    mask = np.zeros((H, nq, n), dtype=bool)
+    for h in range(H):
+        for r in range(nq):
+            order, mass = cdf_order_and_mass(s[h, r])
+            k = int(np.argmax(mass >= tau)) + 1
+            mask[h, r, order[:k]] = True
+            for j in forced_blocks(i0 + r, G):
+                mask[h, r, j] = True
+    counts = mask.sum(axis=2).astype(np.int32)
+    sel = np.full((H, nq, n), -1, dtype=np.int32)
+    for h in range(H):
+        for r in range(nq):
+            idx = np.nonzero(mask[h, r])[0]
+            sel[h, r, :idx.size] = idx
+    return mask, sel, counts
