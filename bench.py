@@ -120,6 +120,18 @@ def attention_flops(sel, L, block, i0, d):
     return int(4 * d * (kv * ci[None, :]).sum())
 
 
+def attention_flops_sel(sel, L, block, i0, d):
+    """attention_flops for a sel padded with -1 (CDF mode): padded entries count nothing."""
+    import numpy as np
+    n = -(-L // block)
+    c = np.minimum(block, L - block * np.arange(n)).astype(np.int64)
+    c_pad = np.concatenate([c, [0]])
+    H, nq, _ = sel.shape
+    kv = c_pad[np.where(sel >= 0, sel, n)].sum(axis=2)
+    ci = c[i0:i0 + nq]
+    return int(4 * d * (kv * ci[None, :]).sum())
+
+
 def gather_bytes(slot_of, L, block, d, w):
     """Algorithmic bytes of the compaction: read valid K and V rows, write whole packed blocks."""
     import numpy as np
@@ -290,6 +302,44 @@ def measure_placement(sp, g, wl, Q, K, V, bufs, packed, stream, ranks_list=(4, 8
     return res
 
 
+def measure_cdf(sp, g, wl, Q, bufs, packed, stream, taus=(0.85, 0.9, 0.95)):
+    """CDF-mode selection (Section 8.1) in place of top-k: the mask kernel's time, the
+    kept blocks per row, and the layer with that selection (scores, CDF mask, demand
+    and gather, attention over the n-wide padded sel)."""
+    import numpy as np
+    import torch
+    res = {}
+    K = packed["_K"]
+    V = packed["_V"]
+    for tau in taus:
+        m, sel, cnt = sp.sparsp_cdf_mask(g, bufs["scores"], tau, wl.global_blocks, stream=stream)
+        t_mask = time_calls(lambda: sp.sparsp_cdf_mask(g, bufs["scores"], tau, wl.global_blocks,
+                                                       mask=m, sel=sel, counts=cnt, stream=stream),
+                            5, stream)
+        c = cnt.cpu().numpy()
+        O = torch.empty((wl.H, wl.nq * wl.block, wl.d), dtype=Q.dtype, device="cuda")
+        cap = wl.H * wl.n
+
+        def layer():
+            sp.sparsp_block_scores(g, Q, K, bufs["pooled_q"], bufs["pooled_k"], bufs["scores"],
+                                   stream=stream)
+            sp.sparsp_cdf_mask(g, bufs["scores"], tau, wl.global_blocks, mask=m, sel=sel,
+                               counts=cnt, stream=stream)
+            sp.sparsp_demand_union_gather(g, m, K, V, cap, out=packed, stream=stream)
+            sp.sparsp_block_sparse_attn(g, Q, sel, packed["slot_of"], packed["K_packed"],
+                                        packed["V_packed"], wl.softmax_scale, O=O, lse=bufs["lse"],
+                                        stream=stream)
+
+        t_layer = time_calls(layer, 3, stream)
+        flops = attention_flops_sel(sel.cpu().numpy(), wl.L, wl.block, wl.i0, wl.d)
+        res[str(tau)] = {"mask_ms": t_mask, "mean_kept_blocks": float(c.mean()),
+                         "min_kept_blocks": int(c.min()), "max_kept_blocks": int(c.max()),
+                         "kept_fraction": float(c.mean()) / wl.n, "layer_ms": t_layer,
+                         "attention_tflop": flops / 1e12,
+                         "layer_tflops": flops / (t_layer * 1e-3) / 1e12}
+    return res
+
+
 def main(argv=None) -> int:
     a = parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -436,6 +486,13 @@ def main(argv=None) -> int:
         c = rec["chunked_attention"]
         log(f"[bench] shard-by-shard: {c['chunks']} chunks {c['chunked_ms']:.3f} ms vs "
             f"{c['unchunked_f32_out_ms']:.3f} ms unchunked; merge {c['merge']['GBps']:.0f} GB/s")
+    if not a.no_extensions and wl.dtype == "bf16":
+        packed["_K"], packed["_V"] = K, V
+        rec["cdf_selection"] = measure_cdf(sp, g, wl, Q, bufs, packed, stream)
+        del packed["_K"], packed["_V"]
+        for tau, v in rec["cdf_selection"].items():
+            log(f"[bench] CDF tau={tau}: {v['mean_kept_blocks']:.1f} blocks/row, mask "
+                f"{v['mask_ms']:.3f} ms, layer {v['layer_ms']:.3f} ms ({v['layer_tflops']:.0f} TFLOP/s)")
     if not a.no_extensions and wl.ranks > 1 and not wl.global_blocks:
         # (reuses the step's packed buffers: runs last)
         rec["placement"] = measure_placement(sp, g, wl, Q, K, V, bufs, packed, stream)

@@ -102,6 +102,26 @@ int sparsp_topk_mask(const sparsp_geom* g, const float* scores, int32_t keep,
                      int32_t* sel, void* stream);
 
 /*
+ * Step 2, CDF mode - the selection rule of the paper's evaluation (Section
+ * 8.1): keep, per query block, the highest-scoring blocks until their
+ * cumulative attention mass reaches tau.
+ *
+ * For local row i of head h: p_j = exp(S[h,i,j] - max_j S) / sum_j exp(...)
+ * over all n blocks (float32); with the blocks ordered by score descending,
+ * then index ascending, the row keeps the shortest prefix whose mass reaches
+ * tau, plus F = {i0+i} U global_blocks. A NaN score has no mass and ranks
+ * last. Scores compare as in sparsp_topk_mask.
+ *
+ * tau in (0, 1]. Outputs: mask uint64 [H, nq, W]; sel int32 [H, nq, n], each
+ * row the kept blocks ascending then -1 (attention skips -1, so pass n as
+ * `keep` with this sel); counts int32 [H, nq], the kept blocks per row.
+ * Errors as for sparsp_topk_mask (no keep), and tau outside (0, 1].
+ */
+int sparsp_cdf_mask(const sparsp_geom* g, const float* scores, float tau,
+                    const int32_t* global_blocks, int32_t n_global, uint64_t* mask, int32_t* sel,
+                    int32_t* counts, void* stream);
+
+/*
  * Step 3 - per-head demand union and compaction (Eq. 2 taken over all owners;
  * Section 5.2: per-head demand, row-major packing, locally derived offsets).
  *

@@ -10,6 +10,7 @@ a tensor is not on the GPU, the call raises.
     sparsp_topk_mask            top-k block mask with forced diagonal (Section 4.1)
     sparsp_demand_union_gather  per-head demand (Eq. 2) and packed K/V (Section 5.2)
     sparsp_block_sparse_attn    attention of the local query blocks (Eq. 1)
+    sparsp_cdf_mask             CDF-mode block mask (Section 8.1), instead of top-k
 
 Shard-by-shard attention (Section 2.3, Section 7):
 
@@ -59,6 +60,8 @@ __all__ = [
     "block_sparse_attn_part",
     "lse_merge",
     "chunked_attn",
+    "sparsp_cdf_mask",
+    "cdf_mask",
     "sparsp_periodic_placement",
     "sparsp_permute_blocks",
     "sparsp_remote_demand",
@@ -155,6 +158,8 @@ _SIGNATURES = {
     "sparsp_chunked_attn": [ctypes.POINTER(_Geom), _VP, _VP, _I32, _VP, _VP, _VP, ctypes.c_int64,
                             ctypes.c_float, ctypes.POINTER(Chunk), _I32, _VP, _VP, _VP],
     "sparsp_periodic_placement": [_I32, _I32, _I32, _I32, _VP, _VP],
+    "sparsp_cdf_mask": [ctypes.POINTER(_Geom), _VP, ctypes.c_float,
+                        ctypes.POINTER(ctypes.c_int32), _I32, _VP, _VP, _VP, _VP],
     "sparsp_permute_blocks": [ctypes.POINTER(_Geom), _VP, _VP, _VP, _I32, _VP],
     "sparsp_remote_demand": [ctypes.POINTER(_Geom), _VP, ctypes.POINTER(ctypes.c_int64),
                              ctypes.POINTER(ctypes.c_int64)],
@@ -276,6 +281,29 @@ def sparsp_topk_mask(geom: Geometry, scores, keep: int, global_blocks: Sequence[
     gs = g.c_struct()
     _check(load_library().sparsp_topk_mask(ctypes.byref(gs), *args, _stream(stream, scores.device)))
     return m, s
+
+
+def sparsp_cdf_mask(geom: Geometry, scores, tau: float, global_blocks: Sequence[int] = (),
+                    mask=None, sel=None, counts=None, stream=None):
+    """CDF-mode block mask. Returns (mask [H,nq,W], sel int32 [H,nq,n] padded with -1,
+    counts int32 [H,nq]); pass sel (its width n is the `keep`) to attention as usual."""
+    torch = _torch()
+    g = geom
+    m = mask if mask is not None else _empty((g.H, g.nq, g.W), torch.int64, scores)
+    s = sel if sel is not None else _empty((g.H, g.nq, g.n), torch.int32, scores)
+    c = counts if counts is not None else _empty((g.H, g.nq), torch.int32, scores)
+    gb = list(int(x) for x in global_blocks)
+    arr = (ctypes.c_int32 * max(1, len(gb)))(*gb)
+    args = (
+        _dev(scores, "scores", torch.float32, (g.H, g.nq, g.n)), ctypes.c_float(float(tau)),
+        arr if gb else None, ctypes.c_int32(len(gb)),
+        _dev(m, "mask", torch.int64, (g.H, g.nq, g.W)),
+        _dev(s, "sel", torch.int32, (g.H, g.nq, g.n)),
+        _dev(c, "counts", torch.int32, (g.H, g.nq)),
+    )
+    gs = g.c_struct()
+    _check(load_library().sparsp_cdf_mask(ctypes.byref(gs), *args, _stream(stream, scores.device)))
+    return m, s, c
 
 
 def sparsp_demand_union_gather(geom: Geometry, mask, K, V, capacity_blocks: Optional[int] = None,
@@ -513,6 +541,7 @@ chunk_plan = sparsp_chunk_plan
 block_sparse_attn_part = sparsp_block_sparse_attn_part
 lse_merge = sparsp_lse_merge
 chunked_attn = sparsp_chunked_attn
+cdf_mask = sparsp_cdf_mask
 periodic_placement = sparsp_periodic_placement
 permute_blocks = sparsp_permute_blocks
 remote_demand = sparsp_remote_demand

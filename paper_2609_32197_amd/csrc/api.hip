@@ -78,6 +78,24 @@ int check_chunked(const sparsp::Geom& G) {
     return SPARSP_OK;
 }
 
+// The forced global blocks as a bitset (host array of n_global indices).
+int global_set(const sparsp::Geom& G, const int32_t* global_blocks, int n_global,
+               sparsp::GlobalSet* gs) {
+    if (n_global < 0 || (n_global > 0 && !global_blocks))
+        return fail(SPARSP_E_INVALID, "global_blocks is NULL but n_global = %d", n_global);
+    if (n_global > sparsp::kMaxGlobal)
+        return fail(SPARSP_E_UNSUPPORTED, "n_global = %d exceeds %d", n_global, sparsp::kMaxGlobal);
+    memset(gs, 0, sizeof(*gs));
+    for (int t = 0; t < n_global; ++t) {
+        const int j = global_blocks[t];
+        if (j < 0 || j >= G.n)
+            return fail(SPARSP_E_INVALID, "global block %d outside [0, %d)", j, G.n);
+        gs->w[j >> 6] |= uint64_t(1) << (j & 63);
+    }
+    for (int w = 0; w < sparsp::kMaxWords; ++w) gs->count += __builtin_popcountll(gs->w[w]);
+    return SPARSP_OK;
+}
+
 // Checks shared by every attention entry point (not the output buffers).
 int check_attn(const sparsp::Geom& G, const void* Q, const int32_t* sel, int keep,
                const int32_t* slot_of, const void* Kp, const void* Vp, int64_t capacity,
@@ -141,19 +159,8 @@ int sparsp_topk_mask(const sparsp_geom* g, const float* scores, int32_t keep,
     sparsp::Geom G;
     if (int rc = derive(g, &G)) return rc;
     if (!scores || !mask || !sel) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
-    if (n_global < 0 || (n_global > 0 && !global_blocks))
-        return fail(SPARSP_E_INVALID, "global_blocks is NULL but n_global = %d", n_global);
-    if (n_global > sparsp::kMaxGlobal)
-        return fail(SPARSP_E_UNSUPPORTED, "n_global = %d exceeds %d", n_global, sparsp::kMaxGlobal);
     sparsp::GlobalSet gs;
-    memset(&gs, 0, sizeof(gs));
-    for (int t = 0; t < n_global; ++t) {
-        const int j = global_blocks[t];
-        if (j < 0 || j >= G.n)
-            return fail(SPARSP_E_INVALID, "global block %d outside [0, %d)", j, G.n);
-        gs.w[j >> 6] |= uint64_t(1) << (j & 63);
-    }
-    for (int w = 0; w < sparsp::kMaxWords; ++w) gs.count += __builtin_popcountll(gs.w[w]);
+    if (int rc = global_set(G, global_blocks, n_global, &gs)) return rc;
     if (keep > G.n) return fail(SPARSP_E_INVALID, "keep = %d exceeds n = %d", keep, G.n);
     // |F_i| = |G| + (i not in G); the largest over local rows bounds keep from below.
     int max_forced = gs.count;
@@ -164,6 +171,19 @@ int sparsp_topk_mask(const sparsp_geom* g, const float* scores, int32_t keep,
                     max_forced);
     hipError_t e = sparsp::launch_topk(G, scores, keep, gs, mask, sel, (hipStream_t)stream);
     return hip_status(e, "sparsp_topk_mask");
+}
+
+int sparsp_cdf_mask(const sparsp_geom* g, const float* scores, float tau,
+                    const int32_t* global_blocks, int32_t n_global, uint64_t* mask, int32_t* sel,
+                    int32_t* counts, void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!scores || !mask || !sel || !counts) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (!(tau > 0.0f && tau <= 1.0f)) return fail(SPARSP_E_INVALID, "tau must be in (0, 1]");
+    sparsp::GlobalSet gs;
+    if (int rc = global_set(G, global_blocks, n_global, &gs)) return rc;
+    hipError_t e = sparsp::launch_cdf(G, scores, tau, gs, mask, sel, counts, (hipStream_t)stream);
+    return hip_status(e, "sparsp_cdf_mask");
 }
 
 int sparsp_demand_union_gather(const sparsp_geom* g, const uint64_t* mask, const void* K,

@@ -33,6 +33,9 @@ hipError_t launch_pool_scores(const Geom& g, const void* Q, const void* K, float
 hipError_t launch_topk(const Geom& g, const float* scores, int keep, const GlobalSet& gs,
                        uint64_t* mask, int32_t* sel, hipStream_t s);
 
+hipError_t launch_cdf(const Geom& g, const float* scores, float tau, const GlobalSet& gs,
+                      uint64_t* mask, int32_t* sel, int32_t* counts, hipStream_t s);
+
 hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void* K, const void* V,
                                 uint64_t* demand, int32_t* head_off, int32_t* slot_of,
                                 int32_t* gather_blk, void* Kp, void* Vp, hipStream_t s);

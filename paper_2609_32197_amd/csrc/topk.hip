@@ -1,5 +1,6 @@
 // Step 2: top-k block mask (Section 4.1's M) with the diagonal and global
-// blocks forced and ties broken by the lower block index.
+// blocks forced and ties broken by the lower block index; and the CDF-mode
+// variant of the mask (Section 8.1), further down.
 //
 // One wave64 per (head, local row). Lane l holds blocks j = l + 64 s
 // (s = 0 .. S-1) in registers, so the 64 lanes of chunk s are exactly the 64
@@ -104,7 +105,129 @@ hipError_t launch_s(const Geom& g, const float* scores, int keep, const GlobalSe
     return hipGetLastError();
 }
 
+// Wave-wide sum and max, the same value in every lane: a butterfly sum can
+// differ in its last bits from lane to lane (each lane adds in its own
+// order), so lane 0's result is broadcast. Every decision below therefore is
+// uniform across the wave.
+__device__ __forceinline__ float wave_sum(float x) {
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+__device__ __forceinline__ float wave_max(float x) {
+    for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+
+// CDF-mode selection (Section 8.1), one wave per (head, local row), blocks held
+// as in topk_kernel. p_j = exp(s_j - max) over the row, Z = sum p. With the
+// blocks ordered by (score desc, index asc), the kept prefix is the shortest
+// one whose mass reaches tau Z: a bitwise search finds the largest order key T
+// whose upper set {key >= T} still holds mass >= tau Z; the blocks above T
+// are kept, and the blocks equal to T (equal scores, equal p) are added in
+// index order until the target is met. The diagonal and global blocks are
+// kept in any case. sel rows list the kept blocks ascending, then -1 up to n.
+// A NaN score counts as no mass and ranks below every number.
+template <int S>
+__global__ __launch_bounds__(256) void cdf_kernel(const float* __restrict__ scores, int H, int nq,
+                                                  int n, int W, int i0, float tau, GlobalSet gs,
+                                                  uint64_t* __restrict__ mask,
+                                                  int32_t* __restrict__ sel,
+                                                  int32_t* __restrict__ counts) {
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= H * nq) return;  // whole wave exits together
+    const int i = i0 + row % nq;
+
+    const float* srow = scores + int64_t(row) * n;
+    uint32_t key[S];
+    float x[S], p[S];
+    bool valid[S], forced[S];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const int j = lane + 64 * s;
+        valid[s] = j < n;
+        forced[s] = valid[s] && (j == i || ((gs.w[s] >> lane) & 1));
+        const float v = valid[s] ? srow[j] : -INFINITY;
+        key[s] = valid[s] ? order_key(v) : 0u;
+        x[s] = (v != v) ? -INFINITY : v;
+        mx = fmaxf(mx, x[s]);
+    }
+    mx = wave_max(mx);
+    float part = 0.f;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        p[s] = (x[s] == -INFINITY) ? 0.f : expf(x[s] - mx);
+        part += p[s];
+    }
+    const float target = tau * wave_sum(part);
+
+    uint32_t T = 0;
+    for (int b = 31; b >= 0; --b) {
+        const uint32_t t = T | (1u << b);
+        float m = 0.f;
+#pragma unroll
+        for (int s = 0; s < S; ++s) m += (valid[s] && key[s] >= t) ? p[s] : 0.f;
+        if (wave_sum(m) >= target) T = t;
+    }
+    float above = 0.f, pt = 0.f;
+    int ties = 0;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        above += (valid[s] && key[s] > T) ? p[s] : 0.f;
+        const bool eq = valid[s] && key[s] == T;
+        pt = fmaxf(pt, eq ? p[s] : 0.f);
+        ties += popc64(__ballot(eq));
+    }
+    float acc = wave_sum(above);
+    pt = wave_max(pt);
+    int need = 0;
+    while (need < ties && acc < target) {  // uniform: every lane holds the same values
+        acc += pt;
+        ++need;
+    }
+
+    uint64_t* mrow = mask + int64_t(row) * W;
+    int32_t* selrow = sel + int64_t(row) * n;
+    int ties_seen = 0, written = 0;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const bool eq = valid[s] && key[s] == T;
+        const uint64_t eqb = __ballot(eq);
+        const bool take_eq = eq && (ties_seen + below_lane(eqb)) < need;
+        ties_seen += popc64(eqb);
+        const bool take = forced[s] || (valid[s] && key[s] > T) || take_eq;
+        const uint64_t word = __ballot(take);
+        if (s < W && lane == 0) mrow[s] = word;
+        if (take) selrow[written + below_lane(word)] = lane + 64 * s;
+        written += popc64(word);
+    }
+    for (int e = written + lane; e < n; e += 64) selrow[e] = -1;
+    if (lane == 0) counts[row] = written;
+}
+
+template <int S>
+hipError_t launch_cdf_s(const Geom& g, const float* scores, float tau, const GlobalSet& gs,
+                        uint64_t* mask, int32_t* sel, int32_t* counts, hipStream_t st) {
+    const int rows = g.H * g.nq;
+    cdf_kernel<S><<<(rows + 3) / 4, 256, 0, st>>>(scores, g.H, g.nq, g.n, g.W, g.i0, tau, gs, mask,
+                                                  sel, counts);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_cdf(const Geom& g, const float* scores, float tau, const GlobalSet& gs,
+                      uint64_t* mask, int32_t* sel, int32_t* counts, hipStream_t st) {
+    (void)hipGetLastError();
+    if (g.W <= 1) return launch_cdf_s<1>(g, scores, tau, gs, mask, sel, counts, st);
+    if (g.W <= 2) return launch_cdf_s<2>(g, scores, tau, gs, mask, sel, counts, st);
+    if (g.W <= 4) return launch_cdf_s<4>(g, scores, tau, gs, mask, sel, counts, st);
+    if (g.W <= 8) return launch_cdf_s<8>(g, scores, tau, gs, mask, sel, counts, st);
+    if (g.W <= 16) return launch_cdf_s<16>(g, scores, tau, gs, mask, sel, counts, st);
+    if (g.W <= 32) return launch_cdf_s<32>(g, scores, tau, gs, mask, sel, counts, st);
+    return launch_cdf_s<64>(g, scores, tau, gs, mask, sel, counts, st);
+}
 
 hipError_t launch_topk(const Geom& g, const float* scores, int keep, const GlobalSet& gs,
                        uint64_t* mask, int32_t* sel, hipStream_t st) {

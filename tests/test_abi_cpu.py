@@ -263,3 +263,17 @@ def test_placement_and_permute_rejected(lib):
     assert lib.sparsp_permute_blocks(ctypes.byref(g), P, P, P, 0, None) == E_INVALID  # X == Y
     assert lib.sparsp_permute_blocks(ctypes.byref(g), P, P, P + 8, 0, None) == E_INVALID
     assert lib.sparsp_permute_blocks(ctypes.byref(g), None, P, P + 4096, 0, None) == E_INVALID
+
+
+def test_cdf_mask_rejected(lib):
+    g = geom(L=1024, block=128, i0=2, i1=6)  # n = 8
+    call = lambda tau, glob=(), ng=None: lib.sparsp_cdf_mask(
+        ctypes.byref(g), P, tau, (ctypes.c_int32 * max(1, len(glob)))(*glob) if glob else None,
+        len(glob) if ng is None else ng, P, P, P, None)
+    assert call(0.0) == E_INVALID
+    assert call(-0.5) == E_INVALID
+    assert call(1.01) == E_INVALID
+    assert call(float("nan")) == E_INVALID
+    assert call(0.9, glob=(8,)) == E_INVALID
+    assert call(0.9, ng=2) == E_INVALID
+    assert lib.sparsp_cdf_mask(ctypes.byref(g), P, 0.9, None, 0, P, P, None, None) == E_INVALID
