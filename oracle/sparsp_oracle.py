@@ -17,6 +17,10 @@ The computation follows the paper (arXiv 2609.32197):
 * Section 5.2: demand is kept per head (not unioned across heads) and blocks
   are packed row-major, each head a contiguous range, so that offsets can be
   derived locally on both ends.
+* Section 5.1: a producer sends each consumer only the blocks of its shard
+  that consumer demands (directly, not relayed around the ring); Section 5.2:
+  per head, packed row-major, offsets derived from the shared mask on both
+  ends;
 * Section 8.1: the evaluation's selection rule (CDF mode) keeps, for each
   query, the highest-scoring key blocks until their cumulative attention mass
   reaches a threshold tau;
@@ -106,6 +110,9 @@ __all__ = [
     "remote_blocks",
     "cdf_order_and_mass",
     "select_cdf",
+    "provide_masks",
+    "pack_by_consumer",
+    "route_volume",
 ]
 
 
@@ -652,3 +659,71 @@ def select_cdf(scores: np.ndarray, tau: float, i0: int, global_blocks: Sequence[
             idx = np.nonzero(mask[h, r])[0]
             sel[h, r, :idx.size] = idx
     return mask, sel, counts
+
+
+# ---------------------------------------------------------------------------
+# Section 5: demand-directed KV routing, producer side
+# ---------------------------------------------------------------------------
+
+def provide_masks(demands: Sequence[np.ndarray], ranks: int, producer: int) -> list:
+    """What producer p sends to each consumer (Eq. 2's D_{c,h,p}), in ring order.
+
+    demands: one bool [H, n] per rank c, the union of c's kept blocks over its
+    query blocks. Returns [(c, bool [H, n])] for c = p+1, ..., p+R-1 (mod R):
+    c's demand restricted to p's shard [floor(p n / R), floor((p+1) n / R)).
+    """
+    H, n = demands[producer].shape
+    lo, hi = local_range(n, ranks, producer)
+    out = []
+    for k in range(1, ranks):
+        c = (producer + k) % ranks
+        m = np.zeros((H, n), dtype=bool)
+        m[:, lo:hi] = demands[c][:, lo:hi]
+        out.append((c, m))
+    return out
+
+
+def pack_by_consumer(provides: Sequence[tuple], K: np.ndarray, V: np.ndarray, L: int,
+                     block: int) -> dict:
+    """Producer-side packing for every consumer, consumers in the given order.
+
+    Each consumer's blocks are packed per head, head-major, block ascending
+    (Section 5.2), consumer after consumer: virtual head v = (consumer index)
+    * H + h. Returns head_off [C*H + 1] (slot offsets of each (consumer, head)
+    run), gather_blk (block per slot), cons_off [C + 1] (first slot of each
+    consumer) and the packed K [slots, block, d] and V (transposed blocks).
+    """
+    H = K.shape[0]
+    C = len(provides)
+    stacked = np.concatenate([m for _, m in provides], axis=0) if C else np.zeros((0, K.shape[1]))
+    head_off, gather_blk, _ = packing_plan(stacked)
+    Kr = np.concatenate([K] * C, axis=0) if C else K[:0]
+    Vr = np.concatenate([V] * C, axis=0) if C else V[:0]
+    Kp, Vp = pack_kv(Kr, Vr, head_off, gather_blk, L, block)
+    cons_off = head_off[::H] if C else np.zeros(1, dtype=head_off.dtype)
+    return {"head_off": head_off, "gather_blk": gather_blk, "cons_off": cons_off,
+            "K_packed": Kp, "V_packed": Vp}
+
+
+def route_volume(provides: Sequence[tuple], shard_blocks: int) -> dict:
+    """Block transfers of one producer's shard under three routings (Section 5.1).
+
+    provides: [(c, bool [H, n])] in ring order (distance 1, 2, ...). Counts, in
+    block-hops summed over heads:
+      dense: the whole shard crosses every one of the R-1 hops;
+      relay: hop k carries the blocks still needed by consumers at distance
+             >= k (the union of their demands);
+      direct: each consumer receives exactly its own blocks once.
+    """
+    C = len(provides)
+    if C == 0:
+        return {"dense": 0, "relay": 0, "direct": 0}
+    H = provides[0][1].shape[0]
+    relay = 0
+    for k in range(C):
+        downstream = np.zeros_like(provides[0][1])
+        for _, m in provides[k:]:
+            downstream |= m
+        relay += int(downstream.sum())
+    direct = int(sum(int(m.sum()) for _, m in provides))
+    return {"dense": C * H * shard_blocks, "relay": relay, "direct": direct}
