@@ -340,6 +340,46 @@ def measure_cdf(sp, g, wl, Q, bufs, packed, stream, taus=(0.85, 0.9, 0.95)):
     return res
 
 
+def measure_routing(sp, g, wl, Q, K, V, packed, stream):
+    """Demand-directed routing (Section 5) at the workload's rank count R: every
+    rank's demand from its own query blocks (contiguous slices), then for each
+    producer the per-consumer packing (sparsp_pack_for_consumers: timed, with its
+    algorithmic bytes) and the dense-ring / relay / direct block-hop counts."""
+    import numpy as np
+    import torch
+    R = wl.ranks
+    dems = []
+    for c in range(R):
+        gr = sp.Geometry(wl.H, wl.L, wl.d, wl.block, (c * wl.n) // R, ((c + 1) * wl.n) // R,
+                         g.dtype)
+        _, _, sc = sp.sparsp_block_scores(gr, Q, K, stream=stream)
+        m, _ = sp.sparsp_topk_mask(gr, sc, wl.keep, wl.global_blocks, stream=stream)
+        sp.sparsp_demand_union_gather(gr, m, K, V, wl.H * wl.n, out=packed, stream=stream)
+        dems.append(packed["demand"].clone())
+    D = torch.stack(dems)
+    c_valid = np.minimum(wl.block, wl.L - wl.block * np.arange(wl.n)).astype(np.int64)
+    row = wl.d * wl.bytes_per_elem
+    per = []
+    for p in range(R):
+        out = sp.sparsp_pack_for_consumers(g, D, R, p, K, V, stream=stream)
+        ms = time_calls(lambda: sp.sparsp_pack_for_consumers(g, D, R, p, K, V, out=out,
+                                                             stream=stream), 3, stream)
+        S = int(out["head_off"][-1].item())
+        blk = out["gather_blk"][:S].cpu().numpy()
+        nbytes = int(2 * row * c_valid[blk].sum() + 2 * S * wl.block * row)
+        vol = sp.sparsp_route_volume(g, D, R, p)
+        per.append({"producer": p, "slots": S, "pack_ms": ms, "bytes": nbytes,
+                    "GBps": nbytes / (ms * 1e-3) / 1e9, **vol})
+        del out
+    blk_bytes = 2 * wl.block * wl.d * wl.bytes_per_elem  # K and V of one block
+    tot = {k: sum(x[k] for x in per) for k in ("dense", "relay", "direct")}
+    return {"ranks": R, "producers": per,
+            "block_hops": tot,
+            "bytes": {k: v * blk_bytes for k, v in tot.items()},
+            "relay_over_direct": tot["relay"] / max(1, tot["direct"]),
+            "dense_over_direct": tot["dense"] / max(1, tot["direct"])}
+
+
 def main(argv=None) -> int:
     a = parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -493,6 +533,13 @@ def main(argv=None) -> int:
         for tau, v in rec["cdf_selection"].items():
             log(f"[bench] CDF tau={tau}: {v['mean_kept_blocks']:.1f} blocks/row, mask "
                 f"{v['mask_ms']:.3f} ms, layer {v['layer_ms']:.3f} ms ({v['layer_tflops']:.0f} TFLOP/s)")
+    if not a.no_extensions and wl.ranks > 1:
+        # (reuses the step's packed buffers: after the measurements that read them)
+        rec["routing"] = measure_routing(sp, g, wl, Q, K, V, packed, stream)
+        rt = rec["routing"]
+        log(f"[bench] routing R={rt['ranks']}: block-hops dense {rt['block_hops']['dense']} relay "
+            f"{rt['block_hops']['relay']} direct {rt['block_hops']['direct']}; pack "
+            f"{np.mean([x['GBps'] for x in rt['producers']]):.0f} GB/s")
     if not a.no_extensions and wl.ranks > 1 and not wl.global_blocks:
         # (reuses the step's packed buffers: runs last)
         rec["placement"] = measure_placement(sp, g, wl, Q, K, V, bufs, packed, stream)

@@ -293,6 +293,45 @@ int sparsp_permute_blocks(const sparsp_geom* g, const int32_t* perm, const void*
 int sparsp_remote_demand(const sparsp_geom* g, const uint64_t* demand, int64_t* remote,
                          int64_t* demanded);
 
+/*
+ * Demand-directed KV routing, producer side (Section 5.1: each consumer gets
+ * exactly the blocks it selected, directly; Section 5.2: per head, packed
+ * row-major, offsets derivable from the shared mask on both ends).
+ *
+ * demands: DEVICE uint64 [ranks, H, W], rank c's demand bitset (the `demand`
+ * output of sparsp_demand_union_gather for c's query blocks). The producer
+ * owns the blocks [floor(producer n / ranks), floor((producer+1) n / ranks)).
+ * Consumers c = producer+1, ..., producer+ranks-1 (mod ranks), in that ring
+ * order, are packed one after another; within a consumer, head-major, block
+ * ascending. With C = ranks - 1 and virtual head v = (distance - 1) * H + h:
+ *   provide   uint64 [C*H, W]  consumer's demand cut to the producer's shard
+ *   head_off  int32 [C*H + 1]  first slot of each (consumer, head) run
+ *   slot_of   int32 [C*H, n]   slot of block j in run v, or -1
+ *   gather_blk int32 [capacity] block of each slot
+ *   K_packed [capacity, block, d], V_packed [capacity, d, block] (transposed)
+ * Consumer c's blocks are slots [head_off[(k-1)*H], head_off[k*H]) for its
+ * distance k; the consumer rebuilds the same offsets from its own demand. The
+ * geometry's local range is not used (it must still be valid). capacity_blocks
+ * must be at least C * H * (shard blocks). Errors: ranks outside [2, n],
+ * producer outside [0, ranks), C * H > 1024, NULL or misaligned pointers.
+ */
+int sparsp_pack_for_consumers(const sparsp_geom* g, const uint64_t* demands, int32_t ranks,
+                              int32_t producer, const void* K, const void* V, uint64_t* provide,
+                              int32_t* head_off, int32_t* slot_of, int32_t* gather_blk,
+                              void* K_packed, void* V_packed, int64_t capacity_blocks,
+                              void* stream);
+
+/*
+ * Block transfers of the producer's shard to the other ranks (Section 5.1),
+ * summed over heads, in block-hops: *dense = the whole shard over each of the
+ * ranks-1 ring hops; *relay = ring forwarding of selected blocks only (hop k
+ * carries what consumers at distance >= k need); *direct = each consumer's
+ * own blocks once. Bytes are 2 * block * d * w per block-hop. demands: HOST
+ * uint64 [ranks, H, W]. Pure host code.
+ */
+int sparsp_route_volume(const sparsp_geom* g, const uint64_t* demands, int32_t ranks,
+                        int32_t producer, int64_t* dense, int64_t* relay, int64_t* direct);
+
 /* Message of the calling thread's most recent error ("" if none). */
 const char* sparsp_last_error(void);
 

@@ -25,6 +25,11 @@ Dependency-aware placement (Section 4.3, Eq. 4):
     sparsp_permute_blocks          token blocks into placed order and back
     sparsp_remote_demand           Eq. 3's remote block count of a rank (host)
 
+Demand-directed KV routing (Section 5):
+
+    sparsp_pack_for_consumers      a producer's packed blocks for every consumer
+    sparsp_route_volume            dense / relay / direct block-hops (host)
+
 Short aliases without the prefix are provided as well.
 """
 
@@ -65,6 +70,10 @@ __all__ = [
     "sparsp_periodic_placement",
     "sparsp_permute_blocks",
     "sparsp_remote_demand",
+    "sparsp_pack_for_consumers",
+    "sparsp_route_volume",
+    "pack_for_consumers",
+    "route_volume",
     "periodic_placement",
     "permute_blocks",
     "remote_demand",
@@ -163,6 +172,11 @@ _SIGNATURES = {
     "sparsp_permute_blocks": [ctypes.POINTER(_Geom), _VP, _VP, _VP, _I32, _VP],
     "sparsp_remote_demand": [ctypes.POINTER(_Geom), _VP, ctypes.POINTER(ctypes.c_int64),
                              ctypes.POINTER(ctypes.c_int64)],
+    "sparsp_pack_for_consumers": [ctypes.POINTER(_Geom), _VP, _I32, _I32, _VP, _VP, _VP, _VP, _VP,
+                                  _VP, _VP, _VP, ctypes.c_int64, _VP],
+    "sparsp_route_volume": [ctypes.POINTER(_Geom), _VP, _I32, _I32,
+                            ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64),
+                            ctypes.POINTER(ctypes.c_int64)],
 }
 
 
@@ -533,6 +547,64 @@ def sparsp_remote_demand(geom: Geometry, demand) -> tuple:
     return rem.value, alld.value
 
 
+# ---------------------------------------------------------------------------
+# demand-directed routing
+# ---------------------------------------------------------------------------
+
+def sparsp_pack_for_consumers(geom: Geometry, demands, ranks: int, producer: int, K, V, out=None,
+                              stream=None):
+    """Producer `producer`'s packed blocks for every other rank, in ring order.
+
+    demands: int64 (uint64 bits) [ranks, H, W] on the GPU. Returns a dict with
+    provide [(R-1)*H, W], head_off [(R-1)*H+1], slot_of [(R-1)*H, n],
+    gather_blk, K_packed, V_packed and capacity_blocks.
+    """
+    torch = _torch()
+    g = geom
+    et = _elem_dtype(g)
+    R = int(ranks)
+    nv = (R - 1) * g.H
+    lo, hi = (int(producer) * g.n) // R, ((int(producer) + 1) * g.n) // R
+    cap = max(1, nv * (hi - lo))
+    o = dict(out or {})
+    o.setdefault("provide", _empty((nv, g.W), torch.int64, K))
+    o.setdefault("head_off", _empty((nv + 1,), torch.int32, K))
+    o.setdefault("slot_of", _empty((nv, g.n), torch.int32, K))
+    o.setdefault("gather_blk", _empty((cap,), torch.int32, K))
+    o.setdefault("K_packed", _empty((cap, g.block, g.d), et, K))
+    o.setdefault("V_packed", _empty((cap, g.d, g.block), et, K))
+    args = (
+        _dev(demands, "demands", torch.int64, (R, g.H, g.W)), R, int(producer),
+        _dev(K, "K", et, (g.H, g.L, g.d)), _dev(V, "V", et, (g.H, g.L, g.d)),
+        _dev(o["provide"], "provide", torch.int64, (nv, g.W)),
+        _dev(o["head_off"], "head_off", torch.int32, (nv + 1,)),
+        _dev(o["slot_of"], "slot_of", torch.int32, (nv, g.n)),
+        _dev(o["gather_blk"], "gather_blk", torch.int32),
+        _dev(o["K_packed"], "K_packed", et), _dev(o["V_packed"], "V_packed", et),
+    )
+    cap = min(o["gather_blk"].numel(), o["K_packed"].shape[0], o["V_packed"].shape[0])
+    gs = g.c_struct()
+    _check(load_library().sparsp_pack_for_consumers(ctypes.byref(gs), *args, ctypes.c_int64(cap),
+                                                   _stream(stream, K.device)))
+    o["capacity_blocks"] = cap
+    return o
+
+
+def sparsp_route_volume(geom: Geometry, demands, ranks: int, producer: int) -> dict:
+    """Block-hops of the producer's shard: {'dense', 'relay', 'direct'} (demands: [R, H, W], any device)."""
+    import numpy as np
+    g = geom
+    if hasattr(demands, "detach"):
+        demands = demands.detach().cpu().numpy()
+    dem = np.ascontiguousarray(np.asarray(demands).view(np.uint64).reshape(int(ranks), g.H, g.W))
+    dense, relay, direct = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    gs = g.c_struct()
+    _check(load_library().sparsp_route_volume(ctypes.byref(gs), dem.ctypes.data, int(ranks),
+                                              int(producer), ctypes.byref(dense),
+                                              ctypes.byref(relay), ctypes.byref(direct)))
+    return {"dense": dense.value, "relay": relay.value, "direct": direct.value}
+
+
 block_scores = sparsp_block_scores
 topk_mask = sparsp_topk_mask
 demand_union_gather = sparsp_demand_union_gather
@@ -545,3 +617,5 @@ cdf_mask = sparsp_cdf_mask
 periodic_placement = sparsp_periodic_placement
 permute_blocks = sparsp_permute_blocks
 remote_demand = sparsp_remote_demand
+pack_for_consumers = sparsp_pack_for_consumers
+route_volume = sparsp_route_volume

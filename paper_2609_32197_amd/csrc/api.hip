@@ -357,4 +357,49 @@ int sparsp_remote_demand(const sparsp_geom* g, const uint64_t* demand, int64_t* 
     return ok();
 }
 
+int sparsp_pack_for_consumers(const sparsp_geom* g, const uint64_t* demands, int32_t ranks,
+                              int32_t producer, const void* K, const void* V, uint64_t* provide,
+                              int32_t* head_off, int32_t* slot_of, int32_t* gather_blk,
+                              void* K_packed, void* V_packed, int64_t capacity_blocks,
+                              void* stream) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!demands || !K || !V || !provide || !head_off || !slot_of || !gather_blk || !K_packed ||
+        !V_packed)
+        return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (ranks < 2 || ranks > G.n)
+        return fail(SPARSP_E_INVALID, "ranks = %d outside [2, n = %d]", ranks, G.n);
+    if (producer < 0 || producer >= ranks)
+        return fail(SPARSP_E_INVALID, "producer = %d outside [0, %d)", producer, ranks);
+    if (int64_t(ranks - 1) * G.H > sparsp::kMaxHeads)
+        return fail(SPARSP_E_UNSUPPORTED, "(ranks-1) * H = %lld exceeds %d",
+                    (long long)(int64_t(ranks - 1) * G.H), sparsp::kMaxHeads);
+    if (int rc = check_chunked(G)) return rc;
+    if (G.block > 4096) return fail(SPARSP_E_UNSUPPORTED, "block %d exceeds 4096", G.block);
+    if (!aligned16(K) || !aligned16(V) || !aligned16(K_packed) || !aligned16(V_packed))
+        return fail(SPARSP_E_INVALID, "K, V and the packed buffers must be 16-byte aligned");
+    const int lo = int(int64_t(producer) * G.n / ranks), hi = int(int64_t(producer + 1) * G.n / ranks);
+    const int64_t need = int64_t(ranks - 1) * G.H * (hi - lo);
+    if (capacity_blocks < need)
+        return fail(SPARSP_E_CAPACITY, "capacity_blocks = %lld < %lld", (long long)capacity_blocks,
+                    (long long)need);
+    hipError_t e = sparsp::launch_pack_for_consumers(G, demands, ranks, producer, lo, hi, K, V,
+                                                     provide, head_off, slot_of, gather_blk,
+                                                     K_packed, V_packed, (hipStream_t)stream);
+    return hip_status(e, "sparsp_pack_for_consumers");
+}
+
+int sparsp_route_volume(const sparsp_geom* g, const uint64_t* demands, int32_t ranks,
+                        int32_t producer, int64_t* dense, int64_t* relay, int64_t* direct) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!demands || !dense || !relay || !direct) return fail(SPARSP_E_INVALID, "NULL pointer");
+    if (ranks < 2 || ranks > G.n)
+        return fail(SPARSP_E_INVALID, "ranks = %d outside [2, n = %d]", ranks, G.n);
+    if (producer < 0 || producer >= ranks)
+        return fail(SPARSP_E_INVALID, "producer = %d outside [0, %d)", producer, ranks);
+    sparsp::route_volume(G, demands, ranks, producer, dense, relay, direct);
+    return ok();
+}
+
 }  // extern "C"

@@ -154,7 +154,8 @@ __global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__
                                                      const char* __restrict__ K,
                                                      const char* __restrict__ V,
                                                      char* __restrict__ Kp, char* __restrict__ Vp,
-                                                     int H, int L, int d, int block, int WS) {
+                                                     int H, int L, int d, int block, int WS,
+                                                     int H_src) {
     constexpr int ES = BF16 ? 2 : 4;  // element size
     constexpr int VEC = 16 / ES;      // elements per 16-byte chunk
     constexpr int T = 256;
@@ -181,7 +182,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__
             const int slot = s0 + tid;
             while (slot >= hoff[h + 1]) ++h;
             const int tok0 = gather_blk[slot] * block;
-            win_src[tid] = (int64_t(h) * L + tok0) * d * ES;
+            win_src[tid] = (int64_t(h % H_src) * L + tok0) * d * ES;
             win_cnt[tid] = min(block, L - tok0);
         }
         __syncthreads();
@@ -252,19 +253,73 @@ hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void*
     if (e != hipSuccess) return e;
     // One workgroup per CU walks the windows (measured best against 128..2048
     // workgroups); the demand total is read on the device, so the grid is fixed.
+    return launch_gather(g, g.H, head_off, gather_blk, K, V, Kp, Vp, s);
+}
+
+// Packed copies of `slots` (virtual) heads: virtual head v reads K/V head v % g.H.
+hipError_t launch_gather(const Geom& g, int n_vheads, const int32_t* head_off,
+                         const int32_t* gather_blk, const void* K, const void* V, void* Kp,
+                         void* Vp, hipStream_t s) {
     const int grid = kGatherGrid;
     const int vec = g.bf16 ? 8 : 4;
     const int v_items = (g.d / vec) * (g.block / vec);  // V sub-blocks per slot
     const int ws = v_items >= 256 ? 1 : min(kMaxWS, (256 + v_items - 1) / v_items);
     if (g.bf16)
         gather_kernel<true><<<grid, 256, 0, s>>>(head_off, gather_blk, (const char*)K,
-                                                 (const char*)V, (char*)Kp, (char*)Vp, g.H, g.L,
-                                                 g.d, g.block, ws);
+                                                 (const char*)V, (char*)Kp, (char*)Vp, n_vheads,
+                                                 g.L, g.d, g.block, ws, g.H);
     else
         gather_kernel<false><<<grid, 256, 0, s>>>(head_off, gather_blk, (const char*)K,
-                                                  (const char*)V, (char*)Kp, (char*)Vp, g.H, g.L,
-                                                  g.d, g.block, ws);
+                                                  (const char*)V, (char*)Kp, (char*)Vp, n_vheads,
+                                                  g.L, g.d, g.block, ws, g.H);
     return hipGetLastError();
+}
+
+// Producer side of demand-directed routing (Section 5.1, Section 5.2): what
+// producer p sends each consumer c = p+1, ..., p+R-1 (ring order) is c's
+// demand cut to p's shard [lo, hi). The cut bitsets are laid out as virtual
+// heads v = (consumer distance - 1) * H + h, after which the offsets and gather
+// kernels above pack every consumer's blocks per head, row-major, consumer
+// after consumer, in one pass.
+__global__ __launch_bounds__(256) void provide_kernel(const uint64_t* __restrict__ demands,
+                                                      int ranks, int producer, int H, int W,
+                                                      int lo, int hi,
+                                                      uint64_t* __restrict__ provide) {
+    const int64_t total = int64_t(ranks - 1) * H * W;
+    for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total;
+         e += int64_t(gridDim.x) * 256) {
+        const int w = int(e % W);
+        const int64_t vh = e / W;
+        const int h = int(vh % H), k = int(vh / H) + 1;
+        const int c = (producer + k) % ranks;
+        // bits of word w inside [lo, hi)
+        const int b0 = w * 64;
+        uint64_t keep = 0;
+        const int from = max(lo, b0), to = min(hi, b0 + 64);
+        if (from < to) {
+            const int len = to - from;
+            keep = (len == 64 ? ~uint64_t(0) : ((uint64_t(1) << len) - 1)) << (from - b0);
+        }
+        provide[e] = demands[(int64_t(c) * H + h) * W + w] & keep;
+    }
+}
+
+hipError_t launch_pack_for_consumers(const Geom& g, const uint64_t* demands, int ranks,
+                                     int producer, int lo, int hi, const void* K, const void* V,
+                                     uint64_t* provide, int32_t* head_off, int32_t* slot_of,
+                                     int32_t* gather_blk, void* Kp, void* Vp, hipStream_t s) {
+    (void)hipGetLastError();
+    const int nv = (ranks - 1) * g.H;
+    const int64_t words = int64_t(nv) * g.W;
+    const int64_t want = (words + 255) / 256;
+    const int grid = int(want < 1024 ? (want > 0 ? want : 1) : 1024);
+    provide_kernel<<<grid, 256, 0, s>>>(demands, ranks, producer, g.H, g.W, lo, hi, provide);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    offsets_kernel<<<nv, 256, 0, s>>>(provide, nv, g.n, g.W, head_off, slot_of, gather_blk);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_gather(g, nv, head_off, gather_blk, K, V, Kp, Vp, s);
 }
 
 }  // namespace sparsp

@@ -16,9 +16,16 @@
 // a malformed perm cannot make the kernel leave the tensors. HBM-bound: it
 // reads and writes H L d w bytes.
 //
+// route_volume (host): the block transfers of producer p's shard (Section
+// 5.1), summed over heads: dense ring forwarding moves the whole shard over
+// each of the R-1 hops; relay forwarding moves, over hop k, the blocks that a
+// consumer at distance >= k still needs; direct delivery moves each
+// consumer's own blocks once.
+//
 // remote_demand (host): sum over heads of the demanded blocks outside the
 // rank's own range [i0, i1) of the geometry, i.e. sum_{p != r} |D_{r,h,p}|
 // of Eq. 3 in the layout (placed or contiguous) the geometry describes.
+#include <algorithm>
 #include <vector>
 
 #include "sparsp_internal.h"
@@ -92,6 +99,31 @@ void remote_demand(const Geom& g, const uint64_t* demand, int64_t* remote, int64
         }
     *remote = rem;
     *demanded = all;
+}
+
+void route_volume(const Geom& g, const uint64_t* demands, int ranks, int producer, int64_t* dense,
+                  int64_t* relay, int64_t* direct) {
+    const int lo = int(int64_t(producer) * g.n / ranks), hi = int(int64_t(producer + 1) * g.n / ranks);
+    int64_t rel = 0, dir = 0;
+    std::vector<uint64_t> down(g.W);
+    for (int h = 0; h < g.H; ++h) {
+        std::fill(down.begin(), down.end(), 0);
+        for (int k = ranks - 1; k >= 1; --k) {  // farthest consumer first: down = union of distance >= k
+            const int c = (producer + k) % ranks;
+            const uint64_t* dm = demands + (int64_t(c) * g.H + h) * g.W;
+            for (int j = lo; j < hi; ++j) {
+                const uint64_t bit = uint64_t(1) << (j & 63);
+                if (dm[j >> 6] & bit) {
+                    ++dir;
+                    down[j >> 6] |= bit;
+                }
+            }
+            for (int j = lo; j < hi; ++j) rel += int64_t((down[j >> 6] >> (j & 63)) & 1);
+        }
+    }
+    *dense = int64_t(ranks - 1) * g.H * (hi - lo);
+    *relay = rel;
+    *direct = dir;
 }
 
 }  // namespace sparsp

@@ -50,6 +50,21 @@ struct AttnPart {
     int kv_lo, kv_hi, h_lo, h_hi, acc;
 };
 
+// Packed K/V copies of n_vheads virtual heads (virtual head v reads head v % g.H).
+hipError_t launch_gather(const Geom& g, int n_vheads, const int32_t* head_off,
+                         const int32_t* gather_blk, const void* K, const void* V, void* Kp,
+                         void* Vp, hipStream_t s);
+
+// Producer p's packing for every other rank (demands: device [ranks, H, W]).
+hipError_t launch_pack_for_consumers(const Geom& g, const uint64_t* demands, int ranks,
+                                     int producer, int lo, int hi, const void* K, const void* V,
+                                     uint64_t* provide, int32_t* head_off, int32_t* slot_of,
+                                     int32_t* gather_blk, void* Kp, void* Vp, hipStream_t s);
+
+// Host: block-hops of producer p's shard under dense ring, relay and direct routing.
+void route_volume(const Geom& g, const uint64_t* demands, int ranks, int producer, int64_t* dense,
+                  int64_t* relay, int64_t* direct);
+
 hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, int keep,
                             const int32_t* slot_of, const void* Kp, const void* Vp,
                             int64_t capacity, float scale, const AttnPart& part, void* O,

@@ -277,3 +277,58 @@ def test_cdf_mask_rejected(lib):
     assert call(0.9, glob=(8,)) == E_INVALID
     assert call(0.9, ng=2) == E_INVALID
     assert lib.sparsp_cdf_mask(ctypes.byref(g), P, 0.9, None, 0, P, P, None, None) == E_INVALID
+
+
+# ---------------------------------------------------------------------------
+# demand-directed routing: the volume counter is host code
+# ---------------------------------------------------------------------------
+
+def test_route_volume_reproduces_the_paper_example(lib):
+    import json
+    import numpy as np
+    import oracle as orc
+    ex = json.load(open(os.path.join(ROOT, "tests", "golden", "cross_ring_example.json")))
+    R, names = ex["ranks"], ex["blocks"]
+    n = R * len(names)
+    dem = [np.zeros((1, n), dtype=bool) for _ in range(R)]
+    for c, blocks in ex["demand"].items():
+        for name in blocks:
+            dem[int(c)][0, names.index(name)] = True
+    words = np.stack([orc.mask_to_words(d) for d in dem])
+    g = sp.Geometry(1, n * 8, 64, 8, 0, 1, sp.F32)
+    vol = sp.sparsp_route_volume(g, words, R, ex["producer"])
+    assert vol["relay"] == ex["relay_block_hops"] and vol["direct"] == ex["direct_blocks"]
+    assert vol["dense"] == (R - 1) * len(names)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_route_volume_matches_the_oracle(lib, seed):
+    import numpy as np
+    import oracle as orc
+    rng = np.random.default_rng(400 + seed)
+    H, n = int(rng.integers(1, 7)), int(rng.integers(2, 200))
+    R = int(rng.integers(2, min(n, 9) + 1))
+    p = int(rng.integers(0, R))
+    demands = [rng.random((H, n)) < rng.uniform(0.05, 0.6) for _ in range(R)]
+    words = np.stack([orc.mask_to_words(d) for d in demands])
+    g = sp.Geometry(H, n * 16, 64, 16, 0, 1, sp.F32)
+    lo, hi = orc.local_range(n, R, p)
+    assert sp.sparsp_route_volume(g, words, R, p) == orc.route_volume(
+        orc.provide_masks(demands, R, p), hi - lo)
+
+
+def test_routing_rejected(lib):
+    g = geom(H=4, L=1024, block=128, i0=0, i1=8)  # n = 8
+    pack = lambda R, p, cap=1 << 20, K=P: lib.sparsp_pack_for_consumers(
+        ctypes.byref(g), P, R, p, K, P, P, P, P, P, P, P, cap, None)
+    assert pack(1, 0) == E_INVALID
+    assert pack(9, 0) == E_INVALID
+    assert pack(4, 4) == E_INVALID
+    assert pack(4, 0, cap=23) == E_CAPACITY  # 3 consumers x 4 heads x 2 shard blocks = 24
+    assert pack(4, 0, K=P + 8) == E_INVALID
+    big = geom(H=300, L=1024, block=128, i0=0, i1=8)
+    assert lib.sparsp_pack_for_consumers(ctypes.byref(big), P, 8, 0, P, P, P, P, P, P, P, P,
+                                         1 << 30, None) == E_UNSUPPORTED  # 7 * 300 > 1024
+    z = ctypes.c_int64()
+    assert lib.sparsp_route_volume(ctypes.byref(g), P, 1, 0, ctypes.byref(z), ctypes.byref(z),
+                                   ctypes.byref(z)) == E_INVALID
