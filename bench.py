@@ -530,9 +530,9 @@ def main(argv=None) -> int:
         packed["_K"], packed["_V"] = K, V
         rec["cdf_selection"] = measure_cdf(sp, g, wl, Q, bufs, packed, stream)
         del packed["_K"], packed["_V"]
-        for tau, v in rec["cdf_selection"].items():
-            log(f"[bench] CDF tau={tau}: {v['mean_kept_blocks']:.1f} blocks/row, mask "
-                f"{v['mask_ms']:.3f} ms, layer {v['layer_ms']:.3f} ms ({v['layer_tflops']:.0f} TFLOP/s)")
+        for tau, res in rec["cdf_selection"].items():
+            log(f"[bench] CDF tau={tau}: {res['mean_kept_blocks']:.1f} blocks/row, mask "
+                f"{res['mask_ms']:.3f} ms, layer {res['layer_ms']:.3f} ms ({res['layer_tflops']:.0f} TFLOP/s)")
     if not a.no_extensions and wl.ranks > 1:
         # (reuses the step's packed buffers: after the measurements that read them)
         rec["routing"] = measure_routing(sp, g, wl, Q, K, V, packed, stream)

@@ -17,7 +17,9 @@
 // (buffer_load_dwordx4 ... lds), double-buffered: the copy of block jj+1 is
 // issued right after the barrier that opens block jj and has the whole of
 // block jj's compute to land; each wave waits for its own copies before the
-// next barrier. One barrier per block. LDS rows carry an XOR
+// next barrier. One barrier per block. Within a block, all MFMA operands of
+// a phase are read from LDS up front (K before the score MFMAs, V^T before
+// the softmax). LDS rows carry an XOR
 // swizzle of their 16-byte chunks (applied through the source addresses of the
 // copies) so the MFMA operand reads are bank-conflict free. Workgroup ids are
 // remapped so that each of the eight XCDs walks a contiguous range of (head,
@@ -115,19 +117,45 @@ __device__ __forceinline__ int chunk_src_offset(int p) {
     return (row * COLS + ((pc ^ swz<COLS>(row)) * 8)) * 2;
 }
 
-// Direct-to-LDS copy of one tile through a buffer resource rooted at the
-// tile: per copy one SGPR base (the LDS destination) and one precomputed VGPR
-// offset. Reads outside the tile return zero instead of faulting.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// Direct-to-LDS copy of one tile (buffer_load_dwordx4 ... lds) through a
+// buffer descriptor rooted at the tile, 16 bytes per lane per instruction:
+// the LDS destination of each instruction is this wave's 1 KB of the tile (in
+// M0), the source a precomputed per-lane offset. Reads outside the tile return
+// zero instead of faulting.
+//
+// The copies are issued as inline assembly on purpose. When the compiler
+// sees direct-to-LDS loads it protects every later LDS read with a wait for
+// all of them, which makes each block wait for the copy of the next one and
+// undoes the double buffering. Issued this way they are invisible to it, and
+// the only wait is the explicit vmcnt(0) that opens each block, which covers
+// exactly the copies issued one block earlier. M0 is saved and restored
+// around the copy; one wait state separates the M0 write from its use.
 template <int NW, int DMA>
 __device__ __forceinline__ void copy_tile(const uint16_t* tile, int tile_bytes, uint16_t* dst,
                                           const int (&voff)[DMA], int wave) {
-#if defined(__HIP_DEVICE_COMPILE__)  // buffer resources exist only in the device pass
-    __amdgpu_buffer_rsrc_t rsrc =
-        __builtin_amdgcn_make_buffer_rsrc((void*)tile, (short)0, tile_bytes, 0x00020000);
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint64_t b = reinterpret_cast<uint64_t>(tile);
+    u32x4_t desc;
+    desc.x = __builtin_amdgcn_readfirstlane(uint32_t(b));
+    desc.y = __builtin_amdgcn_readfirstlane(uint32_t(b >> 32) & 0xffffu);  // stride 0
+    desc.z = uint32_t(tile_bytes);                                         // num_records
+    desc.w = 0x00020000u;
 #pragma unroll
     for (int u = 0; u < DMA; ++u) {
-        uint16_t* d = dst + (u * NW + wave) * 64 * 8;  // this wave's 1 KB of the tile
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)d, 16, voff[u], 0, 0, 0);
+        const uint32_t lds = __builtin_amdgcn_readfirstlane(
+            uint32_t(reinterpret_cast<uintptr_t>(dst + (u * NW + wave) * 64 * 8)));
+        uint32_t saved;
+        asm volatile(
+            "s_mov_b32 %[sv], m0\n\t"
+            "s_mov_b32 m0, %[lds]\n\t"
+            "s_nop 0\n\t"
+            "buffer_load_dwordx4 %[off], %[desc], 0 offen lds\n\t"
+            "s_mov_b32 m0, %[sv]"
+            : [sv] "=&s"(saved)
+            : [lds] "s"(lds), [off] "v"(voff[u]), [desc] "s"(desc)
+            : "memory");
     }
 #endif
 }
@@ -261,18 +289,39 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         for (int mt = 0; mt < C::MTW; ++mt) s[mt] = floatx16{};
         // The score MFMAs run at raised wave priority, so the matrix pipe is
         // fed first while the SIMD's other wave fills in with softmax work.
-        __builtin_amdgcn_s_setprio(1);
+        // All K operands of the block are read from LDS before the first MFMA,
+        // so the LDS latency is paid once per block instead of once per pair
+        // of MFMAs (the scheduler would otherwise sink each read to its use).
+        bf16x8 ka[C::KT][C::MTW];
 #pragma unroll
-        for (int kt = 0; kt < C::KT; ++kt) {
+        for (int kt = 0; kt < C::KT; ++kt)
 #pragma unroll
             for (int mt = 0; mt < C::MTW; ++mt) {
                 const int krow = C::HALF * kh + 32 * mt + sigma(qi);
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                ka[kt][mt] = *reinterpret_cast<const bf16x8*>(
                     lk + krow * D + (((2 * kt + g) ^ swz<D>(krow)) * 8));
-                s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kt], s[mt], 0, 0, 0);
             }
-        }
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt)
+#pragma unroll
+            for (int mt = 0; mt < C::MTW; ++mt)
+                s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kt][mt], qf[kt], s[mt], 0, 0, 0);
         __builtin_amdgcn_s_setprio(0);
+        // The V^T operands of the whole block, read before the softmax so that
+        // the LDS latency overlaps the exponentials.
+        bf16x8 va[C::PTW][C::DT];
+#pragma unroll
+        for (int t = 0; t < C::PTW; ++t)
+#pragma unroll
+            for (int dt = 0; dt < C::DT; ++dt) {
+                const int tg = C::PTW * kh + t;
+                const int vrow = 32 * dt + qi;
+                va[t][dt] = *reinterpret_cast<const bf16x8*>(
+                    lv + vrow * BLK + (((2 * tg + g) ^ swz<BLK>(vrow)) * 8));
+            }
+        __builtin_amdgcn_sched_barrier(0);
         if (cur & 1) {  // partial last block: keys past L do not exist
 #pragma unroll
             for (int mt = 0; mt < C::MTW; ++mt)
@@ -312,14 +361,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 lsum[v & 1] += p[v];
             }
             const bf16x8 pb = __builtin_convertvector(p, bf16x8);
-            const int tg = C::PTW * kh + t;  // 16-key step within the block
 #pragma unroll
-            for (int dt = 0; dt < C::DT; ++dt) {
-                const int vrow = 32 * dt + qi;
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                    lv + vrow * BLK + (((2 * tg + g) ^ swz<BLK>(vrow)) * 8));
-                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, oacc[dt], 0, 0, 0);
-            }
+            for (int dt = 0; dt < C::DT; ++dt)
+                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[t][dt], pb, oacc[dt], 0, 0, 0);
         }
         l_run += lsum[0] + lsum[1];
     }
