@@ -2,24 +2,32 @@
 // the packed K/V buffers (Eq. 1 over the kept blocks; softmax renormalised
 // over the kept keys, computed online in float32).
 //
-// Work split. One workgroup per (head, local query block) with 2*BLK/32
-// waves: wave w owns query group w % (BLK/32) (32 queries) and key half
-// w / (BLK/32) of every kept block (BLK/2 keys). Each wave runs its own online
-// softmax over its key halves (running max, running sum, output accumulator)
-// and the two halves of a query group are merged once at the end through
-// their log-sum-exp, so waves never wait on each other inside a tile. Splitting
-// keys instead of queries halves the LDS bytes each wave reads per tile and
-// keeps two waves per SIMD (256 VGPRs each) to overlap one wave's MFMAs with
-// the other's softmax.
+// Two kernels, one workgroup per (head, local query block) in both; the
+// block size picks the kernel.
 //
-// Data movement. The kept blocks' K tile ([BLK, D]) and transposed V tile
-// ([D, BLK]) are copied HBM -> LDS with direct-to-LDS buffer loads
-// (buffer_load_dwordx4 ... lds), double-buffered: the copy of block jj+1 is
-// issued right after the barrier that opens block jj and has the whole of
-// block jj's compute to land; each wave waits for its own copies before the
-// next barrier. One barrier per block. Within a block, all MFMA operands of
-// a phase are read from LDS up front (K before the score MFMAs, V^T before
-// the softmax). LDS rows carry an XOR
+// attn_b128_kernel (128-token blocks): four waves, wave w owns queries
+// 32 w .. +31 against all 128 keys of every kept block; single K and V tile
+// buffers (64 KB of LDS at d = 128), two workgroups per CU. The waves that
+// share a SIMD come from different workgroups and are not tied by a barrier,
+// so one wave's MFMAs overlap the other's softmax. The copy of the next
+// block's K is issued once the scores of the current block are done, the
+// next V once its output product is done.
+//
+// attn_bf16_kernel (64-token blocks): 2*BLK/32 waves: wave w owns query group
+// w % (BLK/32) (32 queries) and key half w / (BLK/32) of every kept block
+// (BLK/2 keys). Each wave runs its own online softmax over its key halves
+// (running max, running sum, output accumulator) and the two halves of a
+// query group are merged once at the end through their log-sum-exp, so waves
+// never wait on each other inside a tile. Tiles are double-buffered: the copy
+// of block jj+1 is issued right after the barrier that opens block jj and has
+// the whole of block jj's compute to land. One barrier per block.
+//
+// Data movement (both). The kept blocks' K tile ([BLK, D]) and transposed V
+// tile ([D, BLK]) are copied HBM -> LDS with direct-to-LDS buffer loads
+// (buffer_load_dwordx4 ... lds); each wave waits for its own copies before the
+// barrier that publishes them. Within a block, all MFMA operands of a phase
+// are read from LDS up front (K before the score MFMAs, V^T before the
+// softmax). LDS rows carry an XOR
 // swizzle of their 16-byte chunks (applied through the source addresses of the
 // copies) so the MFMA operand reads are bank-conflict free. Workgroup ids are
 // remapped so that each of the eight XCDs walks a contiguous range of (head,
@@ -130,11 +138,14 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 // all of them, which makes each block wait for the copy of the next one and
 // undoes the double buffering. Issued this way they are invisible to it, and
 // the only wait is the explicit vmcnt(0) that opens each block, which covers
-// exactly the copies issued one block earlier. M0 is saved and restored
-// around the copy; one wait state separates the M0 write from its use.
+// exactly the copies issued one block earlier. One assembly block issues all
+// of a lane's copies of the tile, stepping M0 from one destination to the
+// next; M0 is saved and restored around it, and one wait state separates
+// each M0 write from its use.
 template <int NW, int DMA>
 __device__ __forceinline__ void copy_tile(const uint16_t* tile, int tile_bytes, uint16_t* dst,
                                           const int (&voff)[DMA], int wave) {
+    static_assert(DMA == 2 || DMA == 4 || DMA == 8, "copies per lane per tile");
 #if defined(__HIP_DEVICE_COMPILE__)
     const uint64_t b = reinterpret_cast<uint64_t>(tile);
     u32x4_t desc;
@@ -142,21 +153,43 @@ __device__ __forceinline__ void copy_tile(const uint16_t* tile, int tile_bytes, 
     desc.y = __builtin_amdgcn_readfirstlane(uint32_t(b >> 32) & 0xffffu);  // stride 0
     desc.z = uint32_t(tile_bytes);                                         // num_records
     desc.w = 0x00020000u;
-#pragma unroll
-    for (int u = 0; u < DMA; ++u) {
-        const uint32_t lds = __builtin_amdgcn_readfirstlane(
-            uint32_t(reinterpret_cast<uintptr_t>(dst + (u * NW + wave) * 64 * 8)));
-        uint32_t saved;
-        asm volatile(
-            "s_mov_b32 %[sv], m0\n\t"
-            "s_mov_b32 m0, %[lds]\n\t"
-            "s_nop 0\n\t"
-            "buffer_load_dwordx4 %[off], %[desc], 0 offen lds\n\t"
-            "s_mov_b32 m0, %[sv]"
-            : [sv] "=&s"(saved)
-            : [lds] "s"(lds), [off] "v"(voff[u]), [desc] "s"(desc)
-            : "memory");
+    // This wave's first 1 KB of the tile; its next ones follow every NW KB.
+    const uint32_t lds = __builtin_amdgcn_readfirstlane(
+        uint32_t(reinterpret_cast<uintptr_t>(dst + wave * 64 * 8)));
+    constexpr uint32_t kStep = NW * 64 * 16;
+    uint32_t saved;
+#define SPARSP_COPY_HEAD "s_mov_b32 %[sv], m0\n\ts_mov_b32 m0, %[lds]\n\ts_nop 0\n\t"
+#define SPARSP_COPY(o) "buffer_load_dwordx4 %[" #o "], %[desc], 0 offen lds\n\t"
+#define SPARSP_STEP "s_add_u32 m0, m0, %[st]\n\ts_nop 0\n\t"
+#define SPARSP_COPY_TAIL "s_mov_b32 m0, %[sv]"
+    if constexpr (DMA == 2) {
+        asm volatile(SPARSP_COPY_HEAD SPARSP_COPY(o0) SPARSP_STEP SPARSP_COPY(o1) SPARSP_COPY_TAIL
+                     : [sv] "=&s"(saved)
+                     : [lds] "s"(lds), [desc] "s"(desc), [st] "n"(kStep), [o0] "v"(voff[0]),
+                       [o1] "v"(voff[1])
+                     : "memory", "scc");
+    } else if constexpr (DMA == 4) {
+        asm volatile(SPARSP_COPY_HEAD SPARSP_COPY(o0) SPARSP_STEP SPARSP_COPY(o1) SPARSP_STEP
+                         SPARSP_COPY(o2) SPARSP_STEP SPARSP_COPY(o3) SPARSP_COPY_TAIL
+                     : [sv] "=&s"(saved)
+                     : [lds] "s"(lds), [desc] "s"(desc), [st] "n"(kStep), [o0] "v"(voff[0]),
+                       [o1] "v"(voff[1]), [o2] "v"(voff[2]), [o3] "v"(voff[3])
+                     : "memory", "scc");
+    } else {
+        asm volatile(SPARSP_COPY_HEAD SPARSP_COPY(o0) SPARSP_STEP SPARSP_COPY(o1) SPARSP_STEP
+                         SPARSP_COPY(o2) SPARSP_STEP SPARSP_COPY(o3) SPARSP_STEP SPARSP_COPY(o4)
+                             SPARSP_STEP SPARSP_COPY(o5) SPARSP_STEP SPARSP_COPY(o6) SPARSP_STEP
+                                 SPARSP_COPY(o7) SPARSP_COPY_TAIL
+                     : [sv] "=&s"(saved)
+                     : [lds] "s"(lds), [desc] "s"(desc), [st] "n"(kStep), [o0] "v"(voff[0]),
+                       [o1] "v"(voff[1]), [o2] "v"(voff[2]), [o3] "v"(voff[3]),
+                       [o4] "v"(voff[4]), [o5] "v"(voff[5]), [o6] "v"(voff[6]), [o7] "v"(voff[7])
+                     : "memory", "scc");
     }
+#undef SPARSP_COPY_HEAD
+#undef SPARSP_COPY
+#undef SPARSP_STEP
+#undef SPARSP_COPY_TAIL
 #endif
 }
 
@@ -450,6 +483,293 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     if (lse && g == 0 && store) lse[orow] = lse_out;
 }
 
+// Kernel for 128-token blocks: two independent workgroups per CU. Four waves
+// per workgroup, wave w owning queries 32 w .. +31 and every key of each kept
+// block, so each wave runs one online softmax and no merge is needed; single
+// K and V tile buffers (64 KB of LDS at d = 128). The two waves that share a
+// SIMD belong to different workgroups and are not held in step by a common
+// barrier, so one can run its MFMAs while the other runs its softmax. The K
+// copy of block j+1 is issued once every wave has finished the scores of
+// block j, the V copy once the output product of block j is done; each copy
+// thus has half a block of compute to land.
+template <int D>
+struct Cfg128 {
+    static constexpr int BLK = 128;
+    static constexpr int NW = 4;
+    static constexpr int THREADS = 256;
+    static constexpr int KT = D / 16;
+    static constexpr int DT = D / 32;
+    static constexpr int TILE = BLK * D;
+    static constexpr int CHUNKS = TILE / 8;
+    static constexpr int DMA = CHUNKS / THREADS;
+    static_assert(CHUNKS % THREADS == 0, "tile must split evenly");
+};
+
+// s_waitcnt vmcnt(n) for the n copies issued last, other counters untouched.
+template <int N>
+__device__ __forceinline__ void wait_vmem_keep() {
+    static_assert(N >= 0 && N < 16, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+template <int D, bool OUT_BF16>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict__ sel,
+                    const int32_t* __restrict__ slot_of, const uint16_t* __restrict__ Kp,
+                    const uint16_t* __restrict__ Vp, void* __restrict__ O,
+                    float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
+                    int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
+                    int h_lo, int n_heads, int acc, int remap) {
+    using C = Cfg128<D>;
+    constexpr int BLK = 128;
+    __shared__ __attribute__((aligned(16))) uint16_t lk[C::TILE];
+    __shared__ __attribute__((aligned(16))) uint16_t lv[C::TILE];
+    extern __shared__ int32_t codes[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int qi = lane & 31, g = lane >> 5;
+
+    const int G = n_heads * nq;
+    int wg = blockIdx.x;
+    if (remap) {
+        const int xcd = wg & 7, idx = wg >> 3, per = G >> 3, rem = G & 7;
+        wg = xcd * per + min(xcd, rem) + idx;
+    }
+    const int h = h_lo + wg / nq, r = wg % nq;
+    const int qtok = (i0 + r) * BLK + 32 * wave + qi;
+    const bool qvalid = qtok < L;
+
+    __shared__ int wave_cnt[C::NW];
+    int nkeep = 0;
+    {
+        const int32_t* srow = sel + (int64_t(h) * nq + r) * keep;
+        const int32_t* hslot = slot_of + int64_t(h) * n;
+        const bool ragged = (L % BLK) != 0;
+        for (int base = 0; base < keep; base += C::THREADS) {
+            const int jj = base + tid;
+            int code = -1;
+            if (jj < keep) {
+                const int j = srow[jj];
+                if (j >= kv_lo && j < kv_hi && j >= 0 && j < n) {
+                    const int sl = hslot[j];
+                    if (sl >= 0 && sl < capacity && sl < (1 << 30))
+                        code = 2 * sl + ((ragged && j == n - 1) ? 1 : 0);
+                }
+            }
+            const uint64_t bal = __ballot(code >= 0);
+            if (lane == 0) wave_cnt[wave] = __popcll(bal);
+            __syncthreads();
+            int off = nkeep, total = 0;
+#pragma unroll
+            for (int w = 0; w < C::NW; ++w) {
+                off += w < wave ? wave_cnt[w] : 0;
+                total += wave_cnt[w];
+            }
+            const int below = __builtin_amdgcn_mbcnt_hi(
+                uint32_t(bal >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(bal), 0));
+            if (code >= 0) codes[off + below] = code;
+            nkeep += total;
+            __syncthreads();
+        }
+    }
+    if (acc && nkeep == 0) return;
+
+    int kvoff[C::DMA], vvoff[C::DMA];
+#pragma unroll
+    for (int u = 0; u < C::DMA; ++u) {
+        const int p = (u * C::NW + wave) * 64 + lane;
+        kvoff[u] = chunk_src_offset<D>(p);
+        vvoff[u] = chunk_src_offset<BLK>(p);
+    }
+    auto copy_k = [&](int code) {
+        copy_tile<C::NW, C::DMA>(Kp + int64_t(code >> 1) * C::TILE, C::TILE * 2, lk, kvoff, wave);
+    };
+    auto copy_v = [&](int code) {
+        copy_tile<C::NW, C::DMA>(Vp + int64_t(code >> 1) * C::TILE, C::TILE * 2, lv, vvoff, wave);
+    };
+
+    bf16x8 qf[C::KT];
+    {
+        const uint16_t* qp = Q + (int64_t(h) * L + (qvalid ? qtok : 0)) * D + 8 * g;
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt) {
+            uint4 v = qvalid ? *reinterpret_cast<const uint4*>(qp + 16 * kt) : make_uint4(0, 0, 0, 0);
+            qf[kt] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+    // From here on nothing the compiler tracks is in flight: the Q loads are
+    // waited for here, and the copies are issued behind its back (copy_tile).
+    wait_vmem_all();
+    if (nkeep > 0) {
+        copy_k(codes[0]);
+        copy_v(codes[0]);
+    }
+
+    floatx16 oacc[C::DT];
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = floatx16{};
+    float m_run = -INFINITY, l_run = 0.f;
+    const int last_cnt = L - (L / BLK) * BLK;
+
+    // Entering block jj: K(jj) and V(jj) are in flight, K issued first.
+    if (nkeep > 0) {
+        wait_vmem_keep<C::DMA>();  // K(0) landed (V(0) may still be in flight)
+        __syncthreads();
+    }
+    for (int jj = 0; jj < nkeep; ++jj) {
+        const int cur = codes[jj];
+        // Scores: S^T for the wave's 32 queries over all 128 keys of the block;
+        // s[mt][rr] is key 32 mt + 16 (rr/8) + 8 g + rr%8.
+        floatx16 s[4];
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) s[mt] = floatx16{};
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            const int krow = 32 * mt + sigma(qi);
+            bf16x8 ka[C::KT];
+#pragma unroll
+            for (int kt = 0; kt < C::KT; ++kt)
+                ka[kt] = *reinterpret_cast<const bf16x8*>(
+                    lk + krow * D + (((2 * kt + g) ^ swz<D>(krow)) * 8));
+#pragma unroll
+            for (int kt = 0; kt < C::KT; ++kt)
+                s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kt], qf[kt], s[mt], 0, 0, 0);
+        }
+        __builtin_amdgcn_s_setprio(0);
+        wait_vmem_all();   // V(jj) landed
+        __syncthreads();   // V(jj) visible; every wave is done with K(jj)
+        if (jj + 1 < nkeep) copy_k(codes[jj + 1]);
+
+        if (cur & 1) {
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int rr = 0; rr < 16; ++rr) {
+                    const int key = 32 * mt + 16 * (rr >> 3) + 8 * g + (rr & 7);
+                    if (key >= last_cnt) s[mt][rr] = -INFINITY;
+                }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(fmaxf(mx, s[mt][rr]), s[mt][rr + 1]);
+        mx = pair_max(mx) * c2;
+        if (__ballot(mx > m_run + kRescaleThreshold)) {
+            const float m_new = fmaxf(m_run, mx);
+            const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
+        }
+        const float m_use = (m_run == -INFINITY) ? 0.0f : m_run;
+
+        float lsum[2] = {0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {  // 16-key steps
+            const int mt = t >> 1, hf = t & 1;
+            bf16x8 va[C::DT];
+#pragma unroll
+            for (int dt = 0; dt < C::DT; ++dt) {
+                const int vrow = 32 * dt + qi;
+                va[dt] = *reinterpret_cast<const bf16x8*>(
+                    lv + vrow * BLK + (((2 * t + g) ^ swz<BLK>(vrow)) * 8));
+            }
+            floatx8 p;
+#pragma unroll
+            for (int v = 0; v < 8; ++v) {
+                p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, -m_use));
+                lsum[v & 1] += p[v];
+            }
+            const bf16x8 pb = __builtin_convertvector(p, bf16x8);
+#pragma unroll
+            for (int dt = 0; dt < C::DT; ++dt)
+                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[dt], pb, oacc[dt], 0, 0, 0);
+        }
+        l_run += lsum[0] + lsum[1];
+
+        wait_vmem_all();   // K(jj+1) landed
+        __syncthreads();   // K(jj+1) visible; every wave is done with V(jj)
+        if (jj + 1 < nkeep) copy_v(codes[jj + 1]);
+    }
+
+    const float l_tot = pair_sum(l_run);
+    const bool live = qvalid && l_tot > 0.f;
+    const float inv = live ? 1.0f / l_tot : 0.f;
+    const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + 32 * wave + qi;
+    float lse_out = live ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    float ka = 0.f, kb = 1.f;
+    bool store = true;
+    if (!OUT_BF16 && acc) {
+        store = live;
+        if (live) {
+            const float la2 = lse[orow] * kLog2e;
+            const float lb2 = m_run + __log2f(l_tot);
+            const float mm = fmaxf(la2, lb2);
+            const float wa = (la2 == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(la2 - mm);
+            const float wb = __builtin_amdgcn_exp2f(lb2 - mm);
+            const float t = wa + wb;
+            ka = wa / t;
+            kb = wb / t;
+            lse_out = (mm + __log2f(t)) * kLn2;
+        }
+    }
+#pragma unroll
+    for (int dt = 0; dt < C::DT; ++dt) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const int d0 = 32 * dt + 8 * q4 + 4 * g;
+            float o4[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) o4[u] = live ? oacc[dt][4 * q4 + u] * inv : 0.f;
+            if (!store) continue;
+            if constexpr (OUT_BF16) {
+                uint16_t* op = static_cast<uint16_t*>(O) + orow * D + d0;
+                uint2 w;
+                w.x = f32_to_bf16_bits(o4[0]) | (f32_to_bf16_bits(o4[1]) << 16);
+                w.y = f32_to_bf16_bits(o4[2]) | (f32_to_bf16_bits(o4[3]) << 16);
+                *reinterpret_cast<uint2*>(op) = w;
+            } else {
+                float* op = static_cast<float*>(O) + orow * D + d0;
+                if (acc) {
+                    const float4 prev = *reinterpret_cast<const float4*>(op);
+                    o4[0] = ka * prev.x + kb * o4[0];
+                    o4[1] = ka * prev.y + kb * o4[1];
+                    o4[2] = ka * prev.z + kb * o4[2];
+                    o4[3] = ka * prev.w + kb * o4[3];
+                }
+                *reinterpret_cast<float4*>(op) = make_float4(o4[0], o4[1], o4[2], o4[3]);
+            }
+        }
+    }
+    if (lse && g == 0 && store) lse[orow] = lse_out;
+}
+
+template <int D>
+hipError_t launch_b128(const Geom& g, const void* Q, const int32_t* sel, int keep,
+                     const int32_t* slot_of, const void* Kp, const void* Vp, int64_t cap,
+                     float scale, const AttnPart& part, void* O, bool out_bf16, float* lse,
+                     hipStream_t s) {
+    const int n_heads = part.h_hi - part.h_lo;
+    const int G = n_heads * g.nq;
+    const float c2 = scale * kLog2e;
+    const size_t dyn = size_t(keep) * sizeof(int32_t);
+    if (out_bf16)
+        attn_b128_kernel<D, true><<<G, 256, dyn, s>>>(
+            (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
+            g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
+            part.acc, 1);
+    else
+        attn_b128_kernel<D, false><<<G, 256, dyn, s>>>(
+            (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
+            g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
+            part.acc, 1);
+    return hipGetLastError();
+}
+
 template <int D, int BLK>
 hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int keep,
                         const int32_t* slot_of, const void* Kp, const void* Vp, int64_t cap,
@@ -482,16 +802,16 @@ hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, in
                             bool out_bf16, float* lse, hipStream_t s) {
     (void)hipGetLastError();
     if (g.d == 128 && g.block == 128)
-        return launch_shape<128, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
-                                      out_bf16, lse, s);
+        return launch_b128<128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
+                              out_bf16, lse, s);
+    if (g.d == 64 && g.block == 128)
+        return launch_b128<64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
+                             out_bf16, lse, s);
     if (g.d == 64 && g.block == 64)
         return launch_shape<64, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                                     out_bf16, lse, s);
     if (g.d == 128 && g.block == 64)
         return launch_shape<128, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
-                                     out_bf16, lse, s);
-    if (g.d == 64 && g.block == 128)
-        return launch_shape<64, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                                      out_bf16, lse, s);
     return hipErrorInvalidValue;
 }
