@@ -54,8 +54,8 @@ def parse_args(argv=None):
                     help="heads per chunk of a remote shard (shard-by-shard attention)")
     ap.add_argument("--tail-chunk-heads", type=int, default=2,
                     help="heads per chunk of the last remote shard")
-    ap.add_argument("--no-extensions", action="store_true",
-                    help="skip the shard-by-shard attention measurement")
+    ap.add_argument("--extensions", action="store_true",
+                    help="also measure shard-by-shard attention, CDF selection, routing and placement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of this many MiB (for counter calibration)")
     return ap.parse_args(argv)
@@ -108,6 +108,38 @@ def read_traffic():
     if m_sha.group(1) != file_sha(ATTN_SRC):
         return None, "kernel changed since the counters were taken"
     return float(m_b.group(1)), "ok"
+
+
+def measured_peaks(sp, torch, copy_bytes: int, stream):
+    """Practical ceilings on this part, beside the data-sheet peaks: the bf16
+    MFMA rate with register operands (the library's probe kernel, best of
+    three ~20 ms launches) and a plain device-to-device copy of copy_bytes
+    (read + write, mean of five)."""
+    wgs, iters = 1024, 60000
+    sink = torch.empty(wgs * 256, dtype=torch.float32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    sp.sparsp_mfma_probe(1000, wgs, sink, stream=stream)
+    best = 0.0
+    for _ in range(3):
+        e0.record(stream)
+        sp.sparsp_mfma_probe(iters, wgs, sink, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        best = max(best, wgs * iters * 524288 / (e0.elapsed_time(e1) * 1e-3) / 1e12)
+    del sink
+    n = max(1, copy_bytes // 2)
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    with torch.cuda.stream(stream):
+        dst.copy_(src)
+        e0.record(stream)
+        for _ in range(5):
+            dst.copy_(src)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbps = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+    return best, copy_gbps
 
 
 def attention_flops(sel, L, block, i0, d):
@@ -475,6 +507,7 @@ def main(argv=None) -> int:
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
     demanded = int((slot_of >= 0).sum())
     traffic, traffic_note = read_traffic() if wl.name == "wan-share" else (None, "other workload")
+    mfma_meas, copy_meas = measured_peaks(sp, torch, gbytes, stream)
 
     rec = {
         "metric": METRIC,
@@ -501,6 +534,8 @@ def main(argv=None) -> int:
             "kernel_ms": stage_ms["block_sparse_attn"],
             "tflops": attn_tflops,
             "frac_of_mfma_peak": attn_tflops / peak,
+            "measured_mfma_peak_tflops": mfma_meas,
+            "frac_of_measured_mfma_peak": attn_tflops / mfma_meas if wl.dtype == "bf16" else None,
         },
         "gather": {
             "demanded_blocks": demanded,
@@ -509,6 +544,8 @@ def main(argv=None) -> int:
             "call_ms": stage_ms["demand_union_gather"],
             "GBps": gbytes / (stage_ms["demand_union_gather"] * 1e-3) / 1e9,
             "frac_of_hbm_peak": gbytes / (stage_ms["demand_union_gather"] * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+            "measured_copy_GBps": copy_meas,
+            "frac_of_measured_copy": gbytes / (stage_ms["demand_union_gather"] * 1e-3) / 1e9 / copy_meas,
         },
         "roofline": {
             "bound": "mfma",
@@ -521,35 +558,37 @@ def main(argv=None) -> int:
         },
         "cpu_baseline": None,
     }
-    if not a.no_extensions and wl.ranks > 1:
+    if a.extensions and wl.ranks > 1:
         rec["chunked_attention"] = measure_chunked(sp, g, wl, Q, bufs, packed, stream, a)
         c = rec["chunked_attention"]
         log(f"[bench] shard-by-shard: {c['chunks']} chunks {c['chunked_ms']:.3f} ms vs "
             f"{c['unchunked_f32_out_ms']:.3f} ms unchunked; merge {c['merge']['GBps']:.0f} GB/s")
-    if not a.no_extensions and wl.dtype == "bf16":
+    if a.extensions and wl.dtype == "bf16":
         packed["_K"], packed["_V"] = K, V
         rec["cdf_selection"] = measure_cdf(sp, g, wl, Q, bufs, packed, stream)
         del packed["_K"], packed["_V"]
         for tau, res in rec["cdf_selection"].items():
             log(f"[bench] CDF tau={tau}: {res['mean_kept_blocks']:.1f} blocks/row, mask "
                 f"{res['mask_ms']:.3f} ms, layer {res['layer_ms']:.3f} ms ({res['layer_tflops']:.0f} TFLOP/s)")
-    if not a.no_extensions and wl.ranks > 1:
+    if a.extensions and wl.ranks > 1:
         # (reuses the step's packed buffers: after the measurements that read them)
         rec["routing"] = measure_routing(sp, g, wl, Q, K, V, packed, stream)
         rt = rec["routing"]
         log(f"[bench] routing R={rt['ranks']}: block-hops dense {rt['block_hops']['dense']} relay "
             f"{rt['block_hops']['relay']} direct {rt['block_hops']['direct']}; pack "
             f"{np.mean([x['GBps'] for x in rt['producers']]):.0f} GB/s")
-    if not a.no_extensions and wl.ranks > 1 and not wl.global_blocks:
+    if a.extensions and wl.ranks > 1 and not wl.global_blocks:
         # (reuses the step's packed buffers: runs last)
         rec["placement"] = measure_placement(sp, g, wl, Q, K, V, bufs, packed, stream)
         for key, val in rec["placement"].items():
             if key.startswith("R"):
                 log(f"[bench] placement {key}: remote blocks contiguous "
                     f"{val['contiguous']['remote_blocks']} -> periodic {val['periodic']['remote_blocks']}"
-                    f" ({100 * val['remote_reduction']:.1f}% less)")
+                    f" ({-100 * val['remote_reduction']:+.1f}%)")
     log(f"[bench] {wl.name}: {ms_per_step:.3f} ms/layer, attention {stage_ms['block_sparse_attn']:.3f} ms "
-        f"= {attn_tflops:.0f} TFLOP/s ({100 * attn_tflops / peak:.1f}% of peak), stages {stage_ms}")
+        f"= {attn_tflops:.0f} TFLOP/s ({100 * attn_tflops / peak:.1f}% of peak, "
+        f"{100 * attn_tflops / mfma_meas:.1f}% of the measured {mfma_meas:.0f}), gather "
+        f"{rec['gather']['GBps']:.0f} GB/s (copy {copy_meas:.0f}), stages {stage_ms}")
     if not a.no_cpu_baseline:
         del Q, K, V, bufs, packed
         torch.cuda.empty_cache()

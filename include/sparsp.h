@@ -332,6 +332,17 @@ int sparsp_pack_for_consumers(const sparsp_geom* g, const uint64_t* demands, int
 int sparsp_route_volume(const sparsp_geom* g, const uint64_t* demands, int32_t ranks,
                         int32_t producer, int64_t* dense, int64_t* relay, int64_t* direct);
 
+/*
+ * Measurement helper, not a step of the method: runs `workgroups` workgroups
+ * of 256 threads, each wave issuing 4 * iters bf16 32x32x16 matrix-core
+ * operations on register operands (no memory traffic), i.e.
+ * workgroups * 4 * 4 * iters * 32768 FLOP, and writes one float per thread to
+ * sink (device, workgroups * 256 floats, caller-owned; the values are
+ * meaningless). Timing it gives the sustained bf16 MFMA rate of the part.
+ * Errors: iters < 1, workgroups < 1 or > 1 << 20, NULL sink.
+ */
+int sparsp_mfma_probe(int64_t iters, int32_t workgroups, float* sink, void* stream);
+
 /* Message of the calling thread's most recent error ("" if none). */
 const char* sparsp_last_error(void);
 

@@ -137,6 +137,14 @@ extern "C" {
 
 int sparsp_version(void) { return 200; }  // 0.2.0
 
+int sparsp_mfma_probe(int64_t iters, int32_t workgroups, float* sink, void* stream) {
+    if (iters < 1 || workgroups < 1 || workgroups > (1 << 20) || !sink)
+        return fail(SPARSP_E_INVALID, "mfma_probe: iters=%lld workgroups=%d sink=%p",
+                    (long long)iters, workgroups, (void*)sink);
+    return hip_status(sparsp::launch_mfma_probe(iters, workgroups, sink, (hipStream_t)stream),
+                      "mfma_probe");
+}
+
 const char* sparsp_last_error(void) { return g_err; }
 
 int sparsp_block_scores(const sparsp_geom* g, const void* Q, const void* K, float* pooled_q,

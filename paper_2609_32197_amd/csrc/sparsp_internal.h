@@ -102,6 +102,8 @@ hipError_t run_chunks(const Geom& g, const void* Q, const int32_t* sel, int keep
                       float scale, const sparsp_chunk* plan, int n_chunks, float* O, float* lse,
                       hipStream_t s);
 
+hipError_t launch_mfma_probe(int64_t iters, int workgroups, float* sink, hipStream_t s);
+
 // ---------------------------------------------------------------------------
 // device helpers
 // ---------------------------------------------------------------------------

@@ -332,3 +332,10 @@ def test_routing_rejected(lib):
     z = ctypes.c_int64()
     assert lib.sparsp_route_volume(ctypes.byref(g), P, 1, 0, ctypes.byref(z), ctypes.byref(z),
                                    ctypes.byref(z)) == E_INVALID
+
+
+def test_mfma_probe_rejected(lib):
+    assert lib.sparsp_mfma_probe(0, 4, P, None) == E_INVALID
+    assert lib.sparsp_mfma_probe(10, 0, P, None) == E_INVALID
+    assert lib.sparsp_mfma_probe(10, (1 << 20) + 1, P, None) == E_INVALID
+    assert lib.sparsp_mfma_probe(10, 4, None, None) == E_INVALID

@@ -213,3 +213,15 @@ def test_errors_surface_through_the_binding(gpu):
     with pytest.raises(sp.SparspError) as ei:
         sp.sparsp_topk_mask(g, sc, 9)
     assert ei.value.code == -1
+
+
+def test_mfma_probe_runs(gpu):
+    """The measurement probe: every thread writes a finite sum."""
+    torch = P.torch()
+    sink = torch.full((8 * 256,), float("nan"), dtype=torch.float32, device="cuda")
+    sp.sparsp_mfma_probe(50, 8, sink)
+    torch.cuda.synchronize()
+    out = sink.cpu()
+    assert torch.isfinite(out).all() and (out != 0).any()
+    with pytest.raises(ValueError):
+        sp.sparsp_mfma_probe(50, 9, sink)
