@@ -621,22 +621,38 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         const int cur = codes[jj];
         // Scores: S^T for the wave's 32 queries over all 128 keys of the block;
         // s[mt][rr] is key 32 mt + 16 (rr/8) + 8 g + rr%8.
+        // k step outermost, so the four accumulators advance together and no
+        // MFMA waits on the one before it; the K operands of step kt+1 are
+        // read while the four MFMAs of step kt run.
         floatx16 s[4];
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) s[mt] = floatx16{};
-        __builtin_amdgcn_s_setprio(1);
+        bf16x8 kb[2][4];
+        auto kread = [&](int kt, bf16x8 (&dst)[4]) {
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const int krow = 32 * mt + sigma(qi);
-            bf16x8 ka[C::KT];
-#pragma unroll
-            for (int kt = 0; kt < C::KT; ++kt)
-                ka[kt] = *reinterpret_cast<const bf16x8*>(
+            for (int mt = 0; mt < 4; ++mt) {
+                const int krow = 32 * mt + sigma(qi);
+                dst[mt] = *reinterpret_cast<const bf16x8*>(
                     lk + krow * D + (((2 * kt + g) ^ swz<D>(krow)) * 8));
+            }
+        };
+        kread(0, kb[0]);
+        __builtin_amdgcn_s_setprio(1);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int kt = 0; kt < C::KT; ++kt)
-                s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[kt], qf[kt], s[mt], 0, 0, 0);
+        for (int kt = 0; kt < C::KT; ++kt) {
+            if (kt + 1 < C::KT) kread(kt + 1, kb[(kt + 1) & 1]);
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+                s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[kt & 1][mt], qf[kt], s[mt], 0, 0, 0);
         }
+        // Keep that order: the reads of step kt+1 ahead of the MFMAs of step kt.
+#pragma unroll
+        for (int kt = 0; kt < C::KT; ++kt) {
+            if (kt + 1 < C::KT) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                      // MFMAs
+        }
+        __builtin_amdgcn_sched_barrier(0);
         __builtin_amdgcn_s_setprio(0);
         wait_vmem_all();   // V(jj) landed
         __syncthreads();   // V(jj) visible; every wave is done with K(jj)
@@ -667,17 +683,25 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         }
         const float m_use = (m_run == -INFINITY) ? 0.0f : m_run;
 
+        // 16-key steps; the V^T operands of step t+1 are read before the
+        // softmax of step t.
         float lsum[2] = {0.f, 0.f};
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {  // 16-key steps
-            const int mt = t >> 1, hf = t & 1;
-            bf16x8 va[C::DT];
+        bf16x8 vb[2][C::DT];
+        auto vread = [&](int t, bf16x8 (&dst)[C::DT]) {
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt) {
                 const int vrow = 32 * dt + qi;
-                va[dt] = *reinterpret_cast<const bf16x8*>(
+                dst[dt] = *reinterpret_cast<const bf16x8*>(
                     lv + vrow * BLK + (((2 * t + g) ^ swz<BLK>(vrow)) * 8));
             }
+        };
+        vread(0, vb[0]);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int mt = t >> 1, hf = t & 1;
+            if (t + 1 < 8) vread(t + 1, vb[(t + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            bf16x8 (&va)[C::DT] = vb[t & 1];
             floatx8 p;
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
