@@ -239,6 +239,94 @@ __global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__
     }
 }
 
+// Streaming form of the same copy for shapes where one workgroup step stays
+// inside one slot: 1,024 16-byte chunks of a K block and 256 VEC x VEC V
+// sub-blocks (d = 128 with 128-token blocks, either dtype). A grid of two
+// workgroups per CU strides over the packed buffers, so at any moment the
+// workgroups read and write neighbouring pieces of memory, the way a plain
+// streaming copy does; loads and stores are non-temporal (the data is used
+// once, by the next kernel). The V transpose places eight consecutive
+// sub-blocks of a row (VEC * 8 tokens) in eight consecutive lanes, so every
+// store instruction writes whole 128-byte row segments.
+constexpr int kStreamGrid = 512;
+
+__device__ __forceinline__ uint4 load_nt(const char* p) {
+    typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p)));
+}
+__device__ __forceinline__ void store_nt(char* p, uint4 v) {
+    typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void gather_stream_kernel(
+    const int32_t* __restrict__ head_off, const int32_t* __restrict__ gather_blk,
+    const char* __restrict__ K, const char* __restrict__ V, char* __restrict__ Kp,
+    char* __restrict__ Vp, int H, int L, int d, int block, int H_src) {
+    constexpr int ES = BF16 ? 2 : 4;
+    constexpr int VEC = 16 / ES;
+    __shared__ int32_t hoff[kMaxHeads + 1];
+    const int tid = threadIdx.x;
+    for (int i = tid; i <= H; i += 256) hoff[i] = head_off[i];
+    __syncthreads();
+    const int total_slots = hoff[H];
+    const int64_t blk_bytes = int64_t(block) * d * ES;
+    const int row_chunks = d / VEC;
+    const int kper = block * row_chunks / 1024;   // K steps per slot
+    const int kblocks = block / VEC, dblocks = d / VEC;
+    const int vper = kblocks * dblocks / 256;     // V steps per slot
+    const int kgroups = kblocks / 8;
+
+    // K: step u copies chunks [1024 part, +1024) of slot u / kper.
+    int h = 0;
+    const int k_steps = total_slots * kper;
+    for (int u = blockIdx.x; u < k_steps; u += gridDim.x) {
+        const int slot = u / kper, part = u - slot * kper;
+        while (slot >= hoff[h + 1]) ++h;
+        const int tok0 = gather_blk[slot] * block;
+        const int valid = min(block, L - tok0) * row_chunks;
+        const char* src = K + (int64_t(h % H_src) * L + tok0) * d * ES;
+        char* dst = Kp + int64_t(slot) * blk_bytes;
+        uint4 x[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = part * 1024 + i * 256 + tid;
+            x[i] = c < valid ? load_nt(src + int64_t(c) * 16) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) store_nt(dst + (int64_t(part) * 1024 + i * 256 + tid) * 16, x[i]);
+    }
+
+    // V: step u transposes sub-blocks [256 part, +256) of slot u / vper. Sub-block
+    // t of the slot: kb = t % 8 + 8 * ((t / 64) % kgroups), db = (t / 8) % 8 + 8 * ((t / 64) / kgroups).
+    h = 0;
+    const int v_steps = total_slots * vper;
+    for (int u = blockIdx.x; u < v_steps; u += gridDim.x) {
+        const int slot = u / vper, part = u - slot * vper;
+        while (slot >= hoff[h + 1]) ++h;
+        const int tok0 = gather_blk[slot] * block;
+        const int cnt = min(block, L - tok0);
+        const char* src = V + (int64_t(h % H_src) * L + tok0) * d * ES;
+        char* dst = Vp + int64_t(slot) * blk_bytes;
+        const int t = part * 256 + tid;
+        const int grp = t >> 6;
+        const int kb = (t & 7) + 8 * (grp % kgroups);
+        const int db = ((t >> 3) & 7) + 8 * (grp / kgroups);
+        uint4 rows[VEC], cols[VEC];
+#pragma unroll
+        for (int rr = 0; rr < VEC; ++rr) {
+            const int tk = kb * VEC + rr;
+            rows[rr] = tk < cnt ? load_nt(src + (int64_t(tk) * d + db * VEC) * ES) : make_uint4(0, 0, 0, 0);
+        }
+        if constexpr (BF16) transpose8x8_b16(rows, cols);
+        else transpose4x4_b32(rows, cols);
+#pragma unroll
+        for (int c = 0; c < VEC; ++c)
+            store_nt(dst + (int64_t(db * VEC + c) * block + kb * VEC) * ES, cols[c]);
+    }
+}
+
 }  // namespace
 
 hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void* K, const void* V,
@@ -260,9 +348,22 @@ hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void*
 hipError_t launch_gather(const Geom& g, int n_vheads, const int32_t* head_off,
                          const int32_t* gather_blk, const void* K, const void* V, void* Kp,
                          void* Vp, hipStream_t s) {
-    const int grid = kGatherGrid;
     const int vec = g.bf16 ? 8 : 4;
     const int v_items = (g.d / vec) * (g.block / vec);  // V sub-blocks per slot
+    const int k_items = g.block * (g.d / vec);            // K chunks per slot
+    if (k_items % 1024 == 0 && v_items % 256 == 0 && (g.block / vec) % 8 == 0 &&
+        (g.d / vec) % 8 == 0) {
+        if (g.bf16)
+            gather_stream_kernel<true><<<kStreamGrid, 256, 0, s>>>(
+                head_off, gather_blk, (const char*)K, (const char*)V, (char*)Kp, (char*)Vp,
+                n_vheads, g.L, g.d, g.block, g.H);
+        else
+            gather_stream_kernel<false><<<kStreamGrid, 256, 0, s>>>(
+                head_off, gather_blk, (const char*)K, (const char*)V, (char*)Kp, (char*)Vp,
+                n_vheads, g.L, g.d, g.block, g.H);
+        return hipGetLastError();
+    }
+    const int grid = kGatherGrid;
     const int ws = v_items >= 256 ? 1 : min(kMaxWS, (256 + v_items - 1) / v_items);
     if (g.bf16)
         gather_kernel<true><<<grid, 256, 0, s>>>(head_off, gather_blk, (const char*)K,
