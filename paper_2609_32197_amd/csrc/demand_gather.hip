@@ -239,15 +239,16 @@ __global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__
     }
 }
 
-// Streaming form of the same copy for shapes where one workgroup step stays
-// inside one slot: 1,024 16-byte chunks of a K block and 256 VEC x VEC V
-// sub-blocks (d = 128 with 128-token blocks, either dtype). A grid of two
-// workgroups per CU strides over the packed buffers, so at any moment the
-// workgroups read and write neighbouring pieces of memory, the way a plain
-// streaming copy does; loads and stores are non-temporal (the data is used
-// once, by the next kernel). The V transpose places eight consecutive
-// sub-blocks of a row (VEC * 8 tokens) in eight consecutive lanes, so every
-// store instruction writes whole 128-byte row segments.
+// Streaming form of the same copy. A grid of two workgroups per CU strides
+// over the packed buffers as flat arrays, so at any moment the workgroups
+// read and write neighbouring pieces of memory, the way a plain streaming
+// copy does; loads and stores are non-temporal (the data is used once, by
+// the next kernel). K moves in groups of 256 16-byte chunks and V in groups
+// of 64 VEC x VEC sub-blocks (one wave); a group never straddles two slots,
+// which holds when a K block is a multiple of 256 chunks and a V block of 64
+// sub-blocks with 8 | block / VEC and 8 | d / VEC. The V transpose places
+// eight consecutive sub-blocks of a row (8 VEC tokens) in eight consecutive
+// lanes, so every store instruction writes whole 128-byte row segments.
 constexpr int kStreamGrid = 512;
 
 __device__ __forceinline__ uint4 load_nt(const char* p) {
@@ -259,7 +260,7 @@ __device__ __forceinline__ void store_nt(char* p, uint4 v) {
     __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
 }
 
-template <bool BF16>
+template <bool BF16, bool WHOLE>  // WHOLE: a K block is a multiple of 1,024 chunks
 __global__ __launch_bounds__(256) void gather_stream_kernel(
     const int32_t* __restrict__ head_off, const int32_t* __restrict__ gather_blk,
     const char* __restrict__ K, const char* __restrict__ V, char* __restrict__ Kp,
@@ -273,43 +274,79 @@ __global__ __launch_bounds__(256) void gather_stream_kernel(
     const int total_slots = hoff[H];
     const int64_t blk_bytes = int64_t(block) * d * ES;
     const int row_chunks = d / VEC;
-    const int kper = block * row_chunks / 1024;   // K steps per slot
+    const int k_items = block * row_chunks;        // chunks per K block
     const int kblocks = block / VEC, dblocks = d / VEC;
-    const int vper = kblocks * dblocks / 256;     // V steps per slot
+    const int v_items = kblocks * dblocks;         // sub-blocks per V block
     const int kgroups = kblocks / 8;
 
-    // K: step u copies chunks [1024 part, +1024) of slot u / kper.
+    // K: step u covers chunks [1024 u, 1024 u + 1024) of the flat K buffer.
+    // Flat indices fit 31 bits (checked by the launcher).
     int h = 0;
-    const int k_steps = total_slots * kper;
-    for (int u = blockIdx.x; u < k_steps; u += gridDim.x) {
-        const int slot = u / kper, part = u - slot * kper;
-        while (slot >= hoff[h + 1]) ++h;
-        const int tok0 = gather_blk[slot] * block;
-        const int valid = min(block, L - tok0) * row_chunks;
-        const char* src = K + (int64_t(h % H_src) * L + tok0) * d * ES;
-        char* dst = Kp + int64_t(slot) * blk_bytes;
+    const uint32_t k_total = uint32_t(total_slots) * uint32_t(k_items);
+    for (uint32_t e0 = blockIdx.x * 1024u; e0 < k_total; e0 += gridDim.x * 1024u) {
         uint4 x[4];
+        int64_t dst_off[4];
+        // slot and in-slot offset of each group; a group of 256 chunks never
+        // straddles slots and k_items >= 256, so the next group wraps at most once
+        int slot = int(e0 / uint32_t(k_items));
+        int cbase = int(e0 - uint32_t(slot) * uint32_t(k_items));
+        if constexpr (WHOLE) {  // the step lies in one slot
+            while (slot >= hoff[h + 1]) ++h;
+            const int tok0 = gather_blk[slot] * block;
+            const int valid = min(block, L - tok0) * row_chunks;
+            const char* src = K + (int64_t(h % H_src) * L + tok0) * d * ES;
+            char* dst = Kp + int64_t(e0) * 16;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int c = part * 1024 + i * 256 + tid;
-            x[i] = c < valid ? load_nt(src + int64_t(c) * 16) : make_uint4(0, 0, 0, 0);
+            for (int i = 0; i < 4; ++i) {
+                const int c = cbase + i * 256 + tid;
+                x[i] = c < valid ? load_nt(src + int64_t(c) * 16) : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) store_nt(dst + (i * 256 + tid) * 16, x[i]);
+            continue;
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) store_nt(dst + (int64_t(part) * 1024 + i * 256 + tid) * 16, x[i]);
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t eg = e0 + i * 256u;  // first chunk of the group
+            if (i > 0) {
+                cbase += 256;
+                if (cbase >= k_items) {
+                    cbase -= k_items;
+                    ++slot;
+                }
+            }
+            dst_off[i] = -1;
+            x[i] = make_uint4(0, 0, 0, 0);
+            if (eg < k_total) {
+                const int c = cbase + tid;
+                while (slot >= hoff[h + 1]) ++h;
+                const int tok0 = gather_blk[slot] * block;
+                const int valid = min(block, L - tok0) * row_chunks;
+                if (c < valid)
+                    x[i] = load_nt(K + (int64_t(h % H_src) * L + tok0) * d * ES + int64_t(c) * 16);
+                dst_off[i] = int64_t(eg + tid) * 16;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (dst_off[i] >= 0) store_nt(Kp + dst_off[i], x[i]);
     }
 
-    // V: step u transposes sub-blocks [256 part, +256) of slot u / vper. Sub-block
-    // t of the slot: kb = t % 8 + 8 * ((t / 64) % kgroups), db = (t / 8) % 8 + 8 * ((t / 64) / kgroups).
+    // V: step u covers sub-blocks [256 u, 256 u + 256) of the flat V buffer,
+    // one group of 64 per wave. Sub-block t of a slot: kb = t % 8 + 8 ((t / 64)
+    // % kgroups), db = (t / 8) % 8 + 8 ((t / 64) / kgroups).
     h = 0;
-    const int v_steps = total_slots * vper;
-    for (int u = blockIdx.x; u < v_steps; u += gridDim.x) {
-        const int slot = u / vper, part = u - slot * vper;
+    const uint32_t v_total = uint32_t(total_slots) * uint32_t(v_items);
+    for (uint32_t t0 = blockIdx.x * 256u; t0 < v_total; t0 += gridDim.x * 256u) {
+        const uint32_t tt = t0 + tid;
+        if (tt >= v_total) continue;  // whole waves: v_total is a multiple of 64
+        const int slot = int(tt / uint32_t(v_items));
+        const int t = int(tt - uint32_t(slot) * uint32_t(v_items));
         while (slot >= hoff[h + 1]) ++h;
         const int tok0 = gather_blk[slot] * block;
         const int cnt = min(block, L - tok0);
         const char* src = V + (int64_t(h % H_src) * L + tok0) * d * ES;
         char* dst = Vp + int64_t(slot) * blk_bytes;
-        const int t = part * 256 + tid;
         const int grp = t >> 6;
         const int kb = (t & 7) + 8 * (grp % kgroups);
         const int db = ((t >> 3) & 7) + 8 * (grp / kgroups);
@@ -351,16 +388,14 @@ hipError_t launch_gather(const Geom& g, int n_vheads, const int32_t* head_off,
     const int vec = g.bf16 ? 8 : 4;
     const int v_items = (g.d / vec) * (g.block / vec);  // V sub-blocks per slot
     const int k_items = g.block * (g.d / vec);            // K chunks per slot
-    if (k_items % 1024 == 0 && v_items % 256 == 0 && (g.block / vec) % 8 == 0 &&
-        (g.d / vec) % 8 == 0) {
-        if (g.bf16)
-            gather_stream_kernel<true><<<kStreamGrid, 256, 0, s>>>(
-                head_off, gather_blk, (const char*)K, (const char*)V, (char*)Kp, (char*)Vp,
-                n_vheads, g.L, g.d, g.block, g.H);
-        else
-            gather_stream_kernel<false><<<kStreamGrid, 256, 0, s>>>(
-                head_off, gather_blk, (const char*)K, (const char*)V, (char*)Kp, (char*)Vp,
-                n_vheads, g.L, g.d, g.block, g.H);
+    const int64_t max_slots = int64_t(n_vheads) * g.n;
+    if (k_items % 256 == 0 && v_items % 64 == 0 && (g.block / vec) % 8 == 0 &&
+        (g.d / vec) % 8 == 0 && max_slots * k_items + int64_t(kStreamGrid) * 1024 < (int64_t(1) << 31)) {
+        const bool whole = k_items % 1024 == 0;
+        auto* kern = g.bf16 ? (whole ? gather_stream_kernel<true, true> : gather_stream_kernel<true, false>)
+                            : (whole ? gather_stream_kernel<false, true> : gather_stream_kernel<false, false>);
+        kern<<<kStreamGrid, 256, 0, s>>>(head_off, gather_blk, (const char*)K, (const char*)V,
+                                         (char*)Kp, (char*)Vp, n_vheads, g.L, g.d, g.block, g.H);
         return hipGetLastError();
     }
     const int grid = kGatherGrid;
