@@ -95,7 +95,17 @@ def test_topk_mask_bit_exact(gpu, case):
     np.testing.assert_array_equal(sel.cpu().numpy(), osel)
 
 
-@pytest.mark.parametrize("geo", GEOMS, ids=lambda g: "H{}L{}d{}b{}_{}-{}_{}".format(*g))
+# Shapes the streaming gather does not take (a block's rows or columns do not
+# split into groups of eight 16-byte chunks): the windowed gather kernel.
+GATHER_ONLY_GEOMS = [
+    (2, 700, 20, 12, 3, 20, "f32"),    # d / 4 = 5, block / 4 = 3, ragged last block
+    (3, 900, 64, 32, 2, 25, "bf16"),   # block / 8 = 4 sub-blocks per row
+    (2, 1000, 128, 16, 0, 63, "bf16"),  # block / 8 = 2, ragged
+]
+
+
+@pytest.mark.parametrize("geo", GEOMS + GATHER_ONLY_GEOMS,
+                         ids=lambda g: "H{}L{}d{}b{}_{}-{}_{}".format(*g))
 def test_demand_gather_bit_exact(gpu, geo):
     H, L, d, b, i0, i1, dt = geo
     n = -(-L // b)
