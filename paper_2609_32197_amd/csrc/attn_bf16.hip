@@ -637,7 +637,6 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             }
         };
         kread(0, kb[0]);
-        __builtin_amdgcn_s_setprio(1);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int kt = 0; kt < C::KT; ++kt) {
@@ -653,11 +652,14 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                      // MFMAs
         }
         __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_setprio(0);
         wait_vmem_all();   // V(jj) landed
         __syncthreads();   // V(jj) visible; every wave is done with K(jj)
         if (jj + 1 < nkeep) copy_k(codes[jj + 1]);
 
+        // Softmax and output product at raised priority: where the other wave
+        // on the SIMD is in its score MFMAs, this wave's VALU work issues first
+        // and the matrix pipe stays fed by both.
+        __builtin_amdgcn_s_setprio(1);
         if (cur & 1) {
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt)
@@ -713,6 +715,7 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             for (int dt = 0; dt < C::DT; ++dt)
                 oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[dt], pb, oacc[dt], 0, 0, 0);
         }
+        __builtin_amdgcn_s_setprio(0);
         l_run += lsum[0] + lsum[1];
 
         wait_vmem_all();   // K(jj+1) landed
