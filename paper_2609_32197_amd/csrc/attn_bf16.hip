@@ -685,8 +685,7 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         }
         const float m_use = (m_run == -INFINITY) ? 0.0f : m_run;
 
-        // 16-key steps; the V^T operands of step t+1 are read before the
-        // softmax of step t.
+        // 16-key steps; the V^T operands of step t+1 are read one step ahead.
         float lsum[2] = {0.f, 0.f};
         bf16x8 vb[2][C::DT];
         auto vread = [&](int t, bf16x8 (&dst)[C::DT]) {
@@ -697,23 +696,38 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                     lv + vrow * BLK + (((2 * t + g) ^ swz<BLK>(vrow)) * 8));
             }
         };
-        vread(0, vb[0]);
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
+        // Step t+1's probabilities are computed while step t's MFMAs run: the
+        // scheduling groups interleave each MFMA with about seven VALU
+        // instructions of the next step.
+        auto pstep = [&](int t) -> bf16x8 {
             const int mt = t >> 1, hf = t & 1;
-            if (t + 1 < 8) vread(t + 1, vb[(t + 1) & 1]);
-            __builtin_amdgcn_sched_barrier(0);
-            bf16x8 (&va)[C::DT] = vb[t & 1];
             floatx8 p;
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
                 p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, -m_use));
                 lsum[v & 1] += p[v];
             }
-            const bf16x8 pb = __builtin_convertvector(p, bf16x8);
+            return __builtin_convertvector(p, bf16x8);
+        };
+        vread(0, vb[0]);
+        bf16x8 pbn = pstep(0);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            if (t + 1 < 8) vread(t + 1, vb[(t + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            const bf16x8 pb = pbn;
+            if (t + 1 < 8) pbn = pstep(t + 1);
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt)
-                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[dt], pb, oacc[dt], 0, 0, 0);
+                oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vb[t & 1][dt], pb, oacc[dt], 0, 0, 0);
+            if (t + 1 < 8) {
+#pragma unroll
+                for (int k = 0; k < C::DT; ++k) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_setprio(0);
         l_run += lsum[0] + lsum[1];
