@@ -8,15 +8,18 @@
 //                block's slot = head_off[h] + rank of the block in D_h, which
 //                fills slot_of and gather_blk. Both ends of an exchange could
 //                derive these offsets locally from the same bitsets.
-// gather_kernel  a fixed grid (one workgroup per CU) walks the demanded slots
-//                in order, reading the slot count and the slot -> (head, block)
-//                map from head_off and gather_blk on the device, so no host
-//                round trip is needed. K blocks are copied with 16-byte
-//                loads and stores; V blocks are written
-//                transposed ([d, block]) so the attention kernel reads V^T MFMA
-//                operands with contiguous 16-byte loads (each thread moves a
-//                VEC x VEC sub-block and transposes it in registers). Rows past
-//                L are written as zero.
+// gather_stream_kernel / gather_kernel
+//                copy the demanded blocks, reading the slot count and the
+//                slot -> (head, block) map from head_off and gather_blk on the
+//                device, so the grid is fixed and no host round trip is needed.
+//                K blocks are copied with 16-byte loads and stores; V blocks
+//                are written transposed ([d, block]) so the attention kernel
+//                reads V^T MFMA operands with contiguous 16-byte loads (each
+//                thread moves a VEC x VEC sub-block and transposes it in
+//                registers). Rows past L are written as zero. The streaming
+//                kernel strides over the packed buffers as flat arrays (the
+//                usual shapes); the windowed kernel walks the slots in windows
+//                (any other shape).
 #include "sparsp_internal.h"
 
 namespace sparsp {
@@ -24,9 +27,8 @@ namespace {
 
 constexpr int kGatherGrid = 256;  // one workgroup per CU of an MI355X
 
-// Plain loads and stores. Non-temporal stores were measured ~6% faster here,
-// but the attention kernel launched right after did not always see their data
-// (stale tiles on its first run), so the packed buffers are written normally.
+// Plain loads and stores for the windowed kernel (the streaming kernel below
+// uses non-temporal ones).
 __device__ __forceinline__ uint4 load_stream(const char* p) {
     return *reinterpret_cast<const uint4*>(p);
 }
