@@ -362,13 +362,37 @@ def measure_cdf(sp, g, wl, Q, bufs, packed, stream, taus=(0.85, 0.9, 0.95)):
                                         packed["V_packed"], wl.softmax_scale, O=O, lse=bufs["lse"],
                                         stream=stream)
 
+        order = torch.empty((wl.H * wl.nq,), dtype=torch.int32, device="cuda")
+
+        def layer_longest_first():
+            sp.sparsp_block_scores(g, Q, K, bufs["pooled_q"], bufs["pooled_k"], bufs["scores"],
+                                   stream=stream)
+            sp.sparsp_cdf_mask(g, bufs["scores"], tau, wl.global_blocks, mask=m, sel=sel,
+                               counts=cnt, stream=stream)
+            sp.sparsp_demand_union_gather(g, m, K, V, cap, out=packed, stream=stream)
+            sp.sparsp_row_order(g, cnt, order=order, stream=stream)
+            sp.sparsp_block_sparse_attn(g, Q, sel, packed["slot_of"], packed["K_packed"],
+                                        packed["V_packed"], wl.softmax_scale, O=O, lse=bufs["lse"],
+                                        stream=stream, row_order=order)
+
         t_layer = time_calls(layer, 3, stream)
+        t_layer_lf = time_calls(layer_longest_first, 3, stream)
+        attn = lambda ro: sp.sparsp_block_sparse_attn(
+            g, Q, sel, packed["slot_of"], packed["K_packed"], packed["V_packed"], wl.softmax_scale,
+            O=O, lse=bufs["lse"], stream=stream, row_order=ro)
+        t_attn = time_calls(lambda: attn(None), 3, stream)
+        t_attn_lf = time_calls(lambda: attn(order), 3, stream)
         flops = attention_flops_sel(sel.cpu().numpy(), wl.L, wl.block, wl.i0, wl.d)
         res[str(tau)] = {"mask_ms": t_mask, "mean_kept_blocks": float(c.mean()),
                          "min_kept_blocks": int(c.min()), "max_kept_blocks": int(c.max()),
                          "kept_fraction": float(c.mean()) / wl.n, "layer_ms": t_layer,
                          "attention_tflop": flops / 1e12,
-                         "layer_tflops": flops / (t_layer * 1e-3) / 1e12}
+                         "layer_tflops": flops / (t_layer * 1e-3) / 1e12,
+                         "attention_ms": t_attn, "attention_tflops": flops / (t_attn * 1e-3) / 1e12,
+                         "layer_ms_longest_first": t_layer_lf,
+                         "layer_tflops_longest_first": flops / (t_layer_lf * 1e-3) / 1e12,
+                         "attention_ms_longest_first": t_attn_lf,
+                         "attention_tflops_longest_first": flops / (t_attn_lf * 1e-3) / 1e12}
     return res
 
 
@@ -569,7 +593,10 @@ def main(argv=None) -> int:
         del packed["_K"], packed["_V"]
         for tau, res in rec["cdf_selection"].items():
             log(f"[bench] CDF tau={tau}: {res['mean_kept_blocks']:.1f} blocks/row, mask "
-                f"{res['mask_ms']:.3f} ms, layer {res['layer_ms']:.3f} ms ({res['layer_tflops']:.0f} TFLOP/s)")
+                f"{res['mask_ms']:.3f} ms, layer {res['layer_ms']:.3f} ms ({res['layer_tflops']:.0f} TFLOP/s), "
+                f"attention {res['attention_ms']:.3f} ms; longest-first: layer "
+                f"{res['layer_ms_longest_first']:.3f} ms, attention {res['attention_ms_longest_first']:.3f} ms "
+                f"({res['attention_tflops_longest_first']:.0f} TFLOP/s)")
     if a.extensions and wl.ranks > 1:
         # (reuses the step's packed buffers: after the measurements that read them)
         rec["routing"] = measure_routing(sp, g, wl, Q, K, V, packed, stream)

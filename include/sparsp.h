@@ -168,6 +168,41 @@ int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t*
                              void* O, int32_t out_dtype, float* lse, void* stream);
 
 /*
+ * Longest-first row order, for selections whose rows keep different numbers of
+ * blocks (CDF mode, Section 8.1): a row whose kept list is several times the
+ * mean otherwise starts late and sets the attention time alone.
+ *
+ * counts: int32 [H, nq], the kept blocks of each local row (as written by
+ * sparsp_cdf_mask); a count outside [0, n] is clamped into it.
+ * order: int32 [H * nq] out, a permutation of the rows h * nq + r for a
+ * launch whose workgroup w runs on XCD w mod 8:
+ *   - heads, by total count (largest first, then lower index), go to the
+ *     least loaded of eight queues that still has room (H/8 heads each, the
+ *     first H mod 8 queues one more), so a head's rows share one XCD's L2;
+ *   - each queue's rows are sorted by count, largest first (rows of equal
+ *     count in unspecified order);
+ *   - the queues are interleaved round-robin: entry k of queue x is at
+ *     position x + 8k while every queue is longer than k.
+ * Device pointers; one workgroup on `stream`.
+ */
+int sparsp_row_order(const sparsp_geom* g, const int32_t* counts, int32_t* order, void* stream);
+
+/*
+ * sparsp_block_sparse_attn with the local rows launched in the order given by
+ * row_order (int32 [H * nq], a permutation of 0 .. H*nq-1, device): workgroup w
+ * computes row row_order[w], and consecutive workgroups go to different XCDs.
+ * Every row's arithmetic is the same as in sparsp_block_sparse_attn, so the
+ * outputs are identical bit for bit; only the schedule changes. Entries
+ * outside [0, H*nq) are skipped, and rows missing from row_order are not
+ * written. Errors: those of sparsp_block_sparse_attn, and a NULL row_order.
+ */
+int sparsp_block_sparse_attn_ordered(const sparsp_geom* g, const void* Q, const int32_t* sel,
+                                     int32_t keep, const int32_t* slot_of, const void* K_packed,
+                                     const void* V_packed, int64_t capacity_blocks,
+                                     float softmax_scale, const int32_t* row_order, void* O,
+                                     int32_t out_dtype, float* lse, void* stream);
+
+/*
  * Shard-by-shard attention (Section 2.3: a rank attends to one owner's KV
  * shard at a time and folds the partial result in with the online softmax;
  * Section 7: shards are cut into chunks of heads and ordered to shorten the

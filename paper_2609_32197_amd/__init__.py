@@ -178,6 +178,10 @@ _SIGNATURES = {
                             ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64),
                             ctypes.POINTER(ctypes.c_int64)],
     "sparsp_mfma_probe": [ctypes.c_int64, _I32, _VP, _VP],
+    "sparsp_row_order": [ctypes.POINTER(_Geom), _VP, _VP, _VP],
+    "sparsp_block_sparse_attn_ordered": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP, _VP,
+                                         _VP, ctypes.c_int64, ctypes.c_float, _VP, _VP,
+                                         ctypes.c_int32, _VP, _VP],
 }
 
 
@@ -362,8 +366,12 @@ def sparsp_demand_union_gather(geom: Geometry, mask, K, V, capacity_blocks: Opti
 
 def sparsp_block_sparse_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed,
                              softmax_scale: Optional[float] = None, out_dtype: Optional[int] = None,
-                             O=None, lse=None, want_lse: bool = True, stream=None):
-    """Block-sparse attention. Returns (O [H, nq*block, d], lse [H, nq*block] or None)."""
+                             O=None, lse=None, want_lse: bool = True, stream=None, row_order=None):
+    """Block-sparse attention. Returns (O [H, nq*block, d], lse [H, nq*block] or None).
+
+    With row_order (int32 [H*nq], e.g. from sparsp_row_order) the rows are
+    launched in that order (sparsp_block_sparse_attn_ordered); the outputs are
+    the same bit for bit."""
     torch = _torch()
     g = geom
     et = _elem_dtype(g)
@@ -390,9 +398,27 @@ def sparsp_block_sparse_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed
         _dev(ls, "lse", torch.float32, (g.H, g.nq * g.block)) if ls is not None else None,
     )
     gs = g.c_struct()
-    _check(load_library().sparsp_block_sparse_attn(ctypes.byref(gs), *args,
-                                                  _stream(stream, Q.device)))
+    lib = load_library()
+    if row_order is None:
+        _check(lib.sparsp_block_sparse_attn(ctypes.byref(gs), *args, _stream(stream, Q.device)))
+    else:
+        ro = _dev(row_order, "row_order", torch.int32, (g.H * g.nq,))
+        _check(lib.sparsp_block_sparse_attn_ordered(ctypes.byref(gs), *args[:8], ro, *args[8:],
+                                                    _stream(stream, Q.device)))
     return o, ls
+
+
+def sparsp_row_order(geom: Geometry, counts, order=None, stream=None):
+    """Rows h*nq + r sorted by counts (int32 [H, nq]) descending, as int32 [H*nq]."""
+    torch = _torch()
+    g = geom
+    o = order if order is not None else _empty((g.H * g.nq,), torch.int32, counts)
+    gs = g.c_struct()
+    _check(load_library().sparsp_row_order(ctypes.byref(gs),
+                                           _dev(counts, "counts", torch.int32, (g.H, g.nq)),
+                                           _dev(o, "order", torch.int32, (g.H * g.nq,)),
+                                           _stream(stream, counts.device)))
+    return o
 
 
 # ---------------------------------------------------------------------------
@@ -617,6 +643,7 @@ def sparsp_mfma_probe(iters: int, workgroups: int, sink, stream=None) -> None:
 
 
 block_scores = sparsp_block_scores
+row_order = sparsp_row_order
 topk_mask = sparsp_topk_mask
 demand_union_gather = sparsp_demand_union_gather
 block_sparse_attn = sparsp_block_sparse_attn

@@ -131,6 +131,34 @@ int check_part(const sparsp::Geom& G, int kv_lo, int kv_hi, int h_lo, int h_hi) 
     return SPARSP_OK;
 }
 
+int attn_whole(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t keep,
+               const int32_t* slot_of, const void* K_packed, const void* V_packed,
+               int64_t capacity_blocks, float softmax_scale, const int32_t* order, void* O,
+               int32_t out_dtype, float* lse, void* stream, const char* what) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (!O) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    if (int rc = check_attn(G, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                            softmax_scale))
+        return rc;
+    if (!aligned16(O)) return fail(SPARSP_E_INVALID, "O must be 16-byte aligned");
+    if (out_dtype != SPARSP_F32 && out_dtype != SPARSP_BF16)
+        return fail(SPARSP_E_DTYPE, "unknown out_dtype %d", out_dtype);
+    if (!G.bf16 && out_dtype != SPARSP_F32)
+        return fail(SPARSP_E_DTYPE, "f32 inputs produce f32 output only");
+    sparsp::AttnPart whole{0, G.n, 0, G.H, 0};
+    whole.order = order;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e =
+        G.bf16 ? sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed,
+                                          capacity_blocks, softmax_scale, whole, O,
+                                          out_dtype == SPARSP_BF16, lse, s)
+               : sparsp::launch_attn_f32(G, (const float*)Q, sel, keep, slot_of,
+                                         (const float*)K_packed, (const float*)V_packed,
+                                         capacity_blocks, softmax_scale, whole, (float*)O, lse, s);
+    return hip_status(e, what);
+}
+
 }  // namespace
 
 extern "C" {
@@ -216,31 +244,33 @@ int sparsp_demand_union_gather(const sparsp_geom* g, const uint64_t* mask, const
     return hip_status(e, "sparsp_demand_union_gather");
 }
 
+
 int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t keep,
                              const int32_t* slot_of, const void* K_packed, const void* V_packed,
                              int64_t capacity_blocks, float softmax_scale, void* O,
                              int32_t out_dtype, float* lse, void* stream) {
+    return attn_whole(g, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                      softmax_scale, nullptr, O, out_dtype, lse, stream,
+                      "sparsp_block_sparse_attn");
+}
+
+int sparsp_block_sparse_attn_ordered(const sparsp_geom* g, const void* Q, const int32_t* sel,
+                                     int32_t keep, const int32_t* slot_of, const void* K_packed,
+                                     const void* V_packed, int64_t capacity_blocks,
+                                     float softmax_scale, const int32_t* row_order, void* O,
+                                     int32_t out_dtype, float* lse, void* stream) {
+    if (!row_order) return fail(SPARSP_E_INVALID, "row_order is NULL");
+    return attn_whole(g, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                      softmax_scale, row_order, O, out_dtype, lse, stream,
+                      "sparsp_block_sparse_attn_ordered");
+}
+
+int sparsp_row_order(const sparsp_geom* g, const int32_t* counts, int32_t* order, void* stream) {
     sparsp::Geom G;
     if (int rc = derive(g, &G)) return rc;
-    if (!O) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
-    if (int rc = check_attn(G, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
-                            softmax_scale))
-        return rc;
-    if (!aligned16(O)) return fail(SPARSP_E_INVALID, "O must be 16-byte aligned");
-    if (out_dtype != SPARSP_F32 && out_dtype != SPARSP_BF16)
-        return fail(SPARSP_E_DTYPE, "unknown out_dtype %d", out_dtype);
-    if (!G.bf16 && out_dtype != SPARSP_F32)
-        return fail(SPARSP_E_DTYPE, "f32 inputs produce f32 output only");
-    const sparsp::AttnPart whole{0, G.n, 0, G.H, 0};
-    hipStream_t s = (hipStream_t)stream;
-    hipError_t e =
-        G.bf16 ? sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed,
-                                          capacity_blocks, softmax_scale, whole, O,
-                                          out_dtype == SPARSP_BF16, lse, s)
-               : sparsp::launch_attn_f32(G, (const float*)Q, sel, keep, slot_of,
-                                         (const float*)K_packed, (const float*)V_packed,
-                                         capacity_blocks, softmax_scale, whole, (float*)O, lse, s);
-    return hip_status(e, "sparsp_block_sparse_attn");
+    if (!counts || !order) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
+    return hip_status(sparsp::launch_row_order(counts, G.H, G.nq, G.n, order, (hipStream_t)stream),
+                      "sparsp_row_order");
 }
 
 int sparsp_chunk_plan(const sparsp_geom* g, const uint64_t* demand, int32_t ranks, int32_t rank,

@@ -200,7 +200,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                       const uint16_t* __restrict__ Vp, void* __restrict__ O,
                       float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
                       int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
-                      int h_lo, int n_heads, int acc, int remap) {
+                      int h_lo, int n_heads, int acc, int remap,
+                      const int32_t* __restrict__ order) {
     using C = Cfg<D, BLK>;
     // [buffer][K tile | V tile]; reused for the final merge.
     __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][C::TILE];
@@ -215,7 +216,10 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     // Workgroup -> (head, local query block), XCD-contiguous when remap is on.
     const int G = n_heads * nq;
     int wg = blockIdx.x;
-    if (remap) {
+    if (order) {  // an explicit row order (e.g. longest first); no XCD remap
+        wg = order[blockIdx.x];
+        if (wg < 0 || wg >= G) return;
+    } else if (remap) {
         const int xcd = wg & 7, idx = wg >> 3, per = G >> 3, rem = G & 7;
         wg = xcd * per + min(xcd, rem) + idx;
     }
@@ -519,7 +523,8 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                     const uint16_t* __restrict__ Vp, void* __restrict__ O,
                     float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
                     int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
-                    int h_lo, int n_heads, int acc, int remap) {
+                    int h_lo, int n_heads, int acc, int remap,
+                    const int32_t* __restrict__ order) {
     using C = Cfg128<D>;
     constexpr int BLK = 128;
     __shared__ __attribute__((aligned(16))) uint16_t lk[C::TILE];
@@ -532,7 +537,10 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 
     const int G = n_heads * nq;
     int wg = blockIdx.x;
-    if (remap) {
+    if (order) {  // an explicit row order (e.g. longest first); no XCD remap
+        wg = order[blockIdx.x];
+        if (wg < 0 || wg >= G) return;
+    } else if (remap) {
         const int xcd = wg & 7, idx = wg >> 3, per = G >> 3, rem = G & 7;
         wg = xcd * per + min(xcd, rem) + idx;
     }
@@ -802,12 +810,12 @@ hipError_t launch_b128(const Geom& g, const void* Q, const int32_t* sel, int kee
         attn_b128_kernel<D, true><<<G, 256, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, 1);
+            part.acc, 1, part.order);
     else
         attn_b128_kernel<D, false><<<G, 256, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, 1);
+            part.acc, 1, part.order);
     return hipGetLastError();
 }
 
@@ -826,12 +834,12 @@ hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int ke
         attn_bf16_kernel<D, BLK, true><<<G, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, remap);
+            part.acc, remap, part.order);
     else
         attn_bf16_kernel<D, BLK, false><<<G, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, remap);
+            part.acc, remap, part.order);
     return hipGetLastError();
 }
 

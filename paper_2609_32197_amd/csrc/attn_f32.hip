@@ -19,11 +19,16 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     const float* __restrict__ Q, const int32_t* __restrict__ sel, const int32_t* __restrict__ slot_of,
     const float* __restrict__ Kp, const float* __restrict__ Vp, float* __restrict__ O,
     float* __restrict__ lse, int L, int n, int d, int block, int i0, int nq, int keep,
-    int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi, int h_lo, int acc) {
+    int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi, int h_lo, int acc,
+    const int32_t* __restrict__ order, int rows) {
     __shared__ float ks[kKeys][DMAX];
     __shared__ float vs[DMAX][kKeys];
 
-    const int wg = blockIdx.x;
+    int wg = blockIdx.x;
+    if (order) {  // an explicit row order (e.g. longest first)
+        wg = order[blockIdx.x];
+        if (wg < 0 || wg >= rows) return;
+    }
     const int h = h_lo + wg / nq, r = wg % nq;
     const int tid = threadIdx.x;
     const int nthr = blockDim.x;
@@ -124,11 +129,11 @@ hipError_t launch_attn_f32(const Geom& g, const float* Q, const int32_t* sel, in
     if (g.d <= 64)
         attn_f32_kernel<64><<<G, threads, 0, s>>>(Q, sel, slot_of, Kp, Vp, O, lse, g.L, g.n, g.d,
                                                   g.block, g.i0, g.nq, keep, capacity, c2,
-                                                  part.kv_lo, part.kv_hi, part.h_lo, part.acc);
+                                                  part.kv_lo, part.kv_hi, part.h_lo, part.acc, part.order, G);
     else
         attn_f32_kernel<128><<<G, threads, 0, s>>>(Q, sel, slot_of, Kp, Vp, O, lse, g.L, g.n,
                                                    g.d, g.block, g.i0, g.nq, keep, capacity, c2,
-                                                   part.kv_lo, part.kv_hi, part.h_lo, part.acc);
+                                                   part.kv_lo, part.kv_hi, part.h_lo, part.acc, part.order, G);
     return hipGetLastError();
 }
 

@@ -48,6 +48,7 @@ hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void*
 // in the part are left untouched.
 struct AttnPart {
     int kv_lo, kv_hi, h_lo, h_hi, acc;
+    const int32_t* order = nullptr;  // workgroup w takes row order[w] (longest first), if set
 };
 
 // Packed K/V copies of n_vheads virtual heads (virtual head v reads head v % g.H).
@@ -103,6 +104,9 @@ hipError_t run_chunks(const Geom& g, const void* Q, const int32_t* sel, int keep
                       hipStream_t s);
 
 hipError_t launch_mfma_probe(int64_t iters, int workgroups, float* sink, hipStream_t s);
+// Rows (h * nq + r) on eight XCD queues by head, each queue longest first, interleaved.
+hipError_t launch_row_order(const int32_t* counts, int H, int nq, int n, int32_t* order,
+                            hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // device helpers

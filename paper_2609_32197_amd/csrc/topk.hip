@@ -215,6 +215,115 @@ hipError_t launch_cdf_s(const Geom& g, const float* scores, float tau, const Glo
     return hipGetLastError();
 }
 
+// Row order for rows of unequal kept counts (CDF selection), for a launch
+// whose workgroup w runs on XCD w mod 8. One workgroup:
+//   1. totals per head; heads ranked by total (descending, then by index);
+//   2. heads dealt to the eight XCD queues largest first, each to the least
+//      loaded queue that still has room (H/8 heads per queue, the first H mod 8
+//      queues one more), so every head's rows share one XCD's L2 and the
+//      queues carry nearly equal work;
+//   3. each queue's rows sorted by count, largest first (counting sort; rows
+//      of equal count in unspecified order);
+//   4. the queues interleaved: entry k of queue x goes to the position that a
+//      round-robin walk over the queues gives it, i.e. x + 8k while all
+//      queues are that long.
+// A count outside [0, n] is clamped into it.
+constexpr int kXcds = 8;
+
+__global__ __launch_bounds__(1024) void row_order_kernel(const int32_t* __restrict__ counts,
+                                                         int H, int nq, int n,
+                                                         int32_t* __restrict__ order) {
+    __shared__ int start[kMaxBlocks + 1];
+    __shared__ int part[1024];
+    __shared__ int64_t tot[kMaxHeads];
+    __shared__ int rank_of[kMaxHeads];   // head -> rank by total
+    __shared__ int head_at[kMaxHeads];   // rank -> head
+    __shared__ int queue_of[kMaxHeads];  // head -> XCD queue
+    __shared__ int qlen[kXcds];
+    const int tid = threadIdx.x;
+    auto cnt_of = [&](int row) { return min(max(counts[row], 0), n); };
+
+    for (int h = tid; h < H; h += 1024) {
+        int64_t t = 0;
+        for (int r = 0; r < nq; ++r) t += cnt_of(h * nq + r);
+        tot[h] = t;
+    }
+    __syncthreads();
+    for (int h = tid; h < H; h += 1024) {
+        int k = 0;
+        for (int o = 0; o < H; ++o) k += (tot[o] > tot[h]) || (tot[o] == tot[h] && o < h);
+        rank_of[h] = k;
+        head_at[k] = h;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int64_t load[kXcds];
+        int room[kXcds];
+        for (int x = 0; x < kXcds; ++x) {
+            load[x] = 0;
+            room[x] = H / kXcds + (x < H % kXcds ? 1 : 0);
+            qlen[x] = room[x] * nq;
+        }
+        for (int k = 0; k < H; ++k) {
+            const int h = head_at[k];
+            int best = -1;
+            for (int x = 0; x < kXcds; ++x)
+                if (room[x] > 0 && (best < 0 || load[x] < load[best])) best = x;
+            queue_of[h] = best;
+            load[best] += tot[h];
+            --room[best];
+        }
+    }
+    __syncthreads();
+    int ql[kXcds];
+#pragma unroll
+    for (int x = 0; x < kXcds; ++x) ql[x] = qlen[x];
+
+    const int rows = H * nq;
+    const int per = (n + 1 + 1023) / 1024;
+    for (int x = 0; x < kXcds; ++x) {
+        if (ql[x] == 0) continue;
+        for (int c = tid; c <= n; c += 1024) start[c] = 0;
+        __syncthreads();
+        for (int r = tid; r < rows; r += 1024)
+            if (queue_of[r / nq] == x) atomicAdd(&start[cnt_of(r)], 1);
+        __syncthreads();
+        // exclusive scan over the count values n, n-1, ..., 0
+        int local = 0;
+        for (int k = 0; k < per; ++k) {
+            const int idx = tid * per + k;
+            if (idx <= n) local += start[n - idx];
+        }
+        part[tid] = local;
+        __syncthreads();
+        for (int off = 1; off < 1024; off <<= 1) {
+            const int v = tid >= off ? part[tid - off] : 0;
+            __syncthreads();
+            part[tid] += v;
+            __syncthreads();
+        }
+        int run = tid ? part[tid - 1] : 0;
+        for (int k = 0; k < per; ++k) {
+            const int idx = tid * per + k;
+            if (idx <= n) {
+                const int c = start[n - idx];
+                start[n - idx] = run;
+                run += c;
+            }
+        }
+        __syncthreads();
+        for (int r = tid; r < rows; r += 1024) {
+            if (queue_of[r / nq] != x) continue;
+            const int k = atomicAdd(&start[cnt_of(r)], 1);  // place in queue x
+            int pos = 0;  // round-robin position of entry k of queue x
+#pragma unroll
+            for (int y = 0; y < kXcds; ++y) pos += min(k, ql[y]) + (y < x && ql[y] > k ? 1 : 0);
+            order[pos] = r;
+        }
+        __syncthreads();
+    }
+}
+
 }  // namespace
 
 hipError_t launch_cdf(const Geom& g, const float* scores, float tau, const GlobalSet& gs,
@@ -239,6 +348,13 @@ hipError_t launch_topk(const Geom& g, const float* scores, int keep, const Globa
     if (g.W <= 16) return launch_s<16>(g, scores, keep, gs, mask, sel, st);
     if (g.W <= 32) return launch_s<32>(g, scores, keep, gs, mask, sel, st);
     return launch_s<64>(g, scores, keep, gs, mask, sel, st);
+}
+
+hipError_t launch_row_order(const int32_t* counts, int H, int nq, int n, int32_t* order,
+                            hipStream_t st) {
+    (void)hipGetLastError();
+    row_order_kernel<<<1, 1024, 0, st>>>(counts, H, nq, n, order);
+    return hipGetLastError();
 }
 
 }  // namespace sparsp

@@ -339,3 +339,17 @@ def test_mfma_probe_rejected(lib):
     assert lib.sparsp_mfma_probe(10, 0, P, None) == E_INVALID
     assert lib.sparsp_mfma_probe(10, (1 << 20) + 1, P, None) == E_INVALID
     assert lib.sparsp_mfma_probe(10, 4, None, None) == E_INVALID
+
+
+def test_row_order_and_ordered_attention_rejected(lib):
+    g = geom(H=2, L=1024, block=128, i0=0, i1=8)
+    assert lib.sparsp_row_order(ctypes.byref(g), None, P, None) == E_INVALID
+    assert lib.sparsp_row_order(ctypes.byref(g), P, None, None) == E_INVALID
+    bad = geom(H=2, L=1024, block=128, i0=3, i1=3)
+    assert lib.sparsp_row_order(ctypes.byref(bad), P, P, None) == E_INVALID
+    gb = geom(H=2, L=1024, d=128, block=128, i0=0, i1=8, dtype=sp.BF16)
+    attn = lambda order, keep=4: lib.sparsp_block_sparse_attn_ordered(
+        ctypes.byref(gb), P, P, keep, P, P, P, 16, 0.1, order, P, sp.BF16, None, None)
+    assert attn(None) == E_INVALID
+    assert attn(P, keep=0) == E_INVALID
+    assert attn(P, keep=9) == E_INVALID
