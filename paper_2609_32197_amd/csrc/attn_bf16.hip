@@ -5,7 +5,7 @@
 // Two kernels, one workgroup per (head, local query block) in both; the
 // block size picks the kernel.
 //
-// attn_b128_kernel (128-token blocks): four waves, wave w owns queries
+// attn_rows_kernel (128-token blocks): four waves, wave w owns queries
 // 32 w .. +31 against all 128 keys of every kept block; single K and V tile
 // buffers (64 KB of LDS at d = 128), two workgroups per CU. The waves that
 // share a SIMD come from different workgroups and are not tied by a barrier,
@@ -496,11 +496,13 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 // copy of block j+1 is issued once every wave has finished the scores of
 // block j, the V copy once the output product of block j is done; each copy
 // thus has half a block of compute to land.
-template <int D>
-struct Cfg128 {
-    static constexpr int BLK = 128;
-    static constexpr int NW = 4;
-    static constexpr int THREADS = 256;
+template <int D, int BLK_>
+struct CfgRows {
+    static constexpr int BLK = BLK_;
+    static constexpr int NW = BLK / 32;          // one wave per 32 queries
+    static constexpr int THREADS = 64 * NW;
+    static constexpr int MT = BLK / 32;          // 32-key tiles of the score product
+    static constexpr int PT = BLK / 16;          // 16-key steps of the output product
     static constexpr int KT = D / 16;
     static constexpr int DT = D / 32;
     static constexpr int TILE = BLK * D;
@@ -516,17 +518,16 @@ __device__ __forceinline__ void wait_vmem_keep() {
     __builtin_amdgcn_s_waitcnt(0x0F70 | N);
 }
 
-template <int D, bool OUT_BF16>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2)))
-void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict__ sel,
+template <int D, int BLK, bool OUT_BF16>
+__global__ __launch_bounds__(64 * (BLK / 32)) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict__ sel,
                     const int32_t* __restrict__ slot_of, const uint16_t* __restrict__ Kp,
                     const uint16_t* __restrict__ Vp, void* __restrict__ O,
                     float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
                     int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
                     int h_lo, int n_heads, int acc, int remap,
                     const int32_t* __restrict__ order) {
-    using C = Cfg128<D>;
-    constexpr int BLK = 128;
+    using C = CfgRows<D, BLK>;
     __shared__ __attribute__((aligned(16))) uint16_t lk[C::TILE];
     __shared__ __attribute__((aligned(16))) uint16_t lv[C::TILE];
     extern __shared__ int32_t codes[];
@@ -632,13 +633,13 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         // k step outermost, so the four accumulators advance together and no
         // MFMA waits on the one before it; the K operands of step kt+1 are
         // read while the four MFMAs of step kt run.
-        floatx16 s[4];
+        floatx16 s[C::MT];
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) s[mt] = floatx16{};
-        bf16x8 kb[2][4];
-        auto kread = [&](int kt, bf16x8 (&dst)[4]) {
+        for (int mt = 0; mt < C::MT; ++mt) s[mt] = floatx16{};
+        bf16x8 kb[2][C::MT];
+        auto kread = [&](int kt, bf16x8 (&dst)[C::MT]) {
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
+            for (int mt = 0; mt < C::MT; ++mt) {
                 const int krow = 32 * mt + sigma(qi);
                 dst[mt] = *reinterpret_cast<const bf16x8*>(
                     lk + krow * D + (((2 * kt + g) ^ swz<D>(krow)) * 8));
@@ -650,14 +651,14 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         for (int kt = 0; kt < C::KT; ++kt) {
             if (kt + 1 < C::KT) kread(kt + 1, kb[(kt + 1) & 1]);
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
+            for (int mt = 0; mt < C::MT; ++mt)
                 s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[kt & 1][mt], qf[kt], s[mt], 0, 0, 0);
         }
         // Keep that order: the reads of step kt+1 ahead of the MFMAs of step kt.
 #pragma unroll
         for (int kt = 0; kt < C::KT; ++kt) {
-            if (kt + 1 < C::KT) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);  // LDS reads
-            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);                      // MFMAs
+            if (kt + 1 < C::KT) __builtin_amdgcn_sched_group_barrier(0x100, C::MT, 0);  // LDS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, C::MT, 0);                      // MFMAs
         }
         __builtin_amdgcn_sched_barrier(0);
         wait_vmem_all();   // V(jj) landed
@@ -670,7 +671,7 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         __builtin_amdgcn_s_setprio(1);
         if (cur & 1) {
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
+            for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
                 for (int rr = 0; rr < 16; ++rr) {
                     const int key = 32 * mt + 16 * (rr >> 3) + 8 * g + (rr & 7);
@@ -679,7 +680,7 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         }
         float mx = -INFINITY;
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
+        for (int mt = 0; mt < C::MT; ++mt)
 #pragma unroll
             for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(fmaxf(mx, s[mt][rr]), s[mt][rr + 1]);
         mx = pair_max(mx) * c2;
@@ -720,15 +721,15 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         vread(0, vb[0]);
         bf16x8 pbn = pstep(0);
 #pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            if (t + 1 < 8) vread(t + 1, vb[(t + 1) & 1]);
+        for (int t = 0; t < C::PT; ++t) {
+            if (t + 1 < C::PT) vread(t + 1, vb[(t + 1) & 1]);
             __builtin_amdgcn_sched_barrier(0);
             const bf16x8 pb = pbn;
-            if (t + 1 < 8) pbn = pstep(t + 1);
+            if (t + 1 < C::PT) pbn = pstep(t + 1);
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt)
                 oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vb[t & 1][dt], pb, oacc[dt], 0, 0, 0);
-            if (t + 1 < 8) {
+            if (t + 1 < C::PT) {
 #pragma unroll
                 for (int k = 0; k < C::DT; ++k) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -797,8 +798,8 @@ void attn_b128_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     if (lse && g == 0 && store) lse[orow] = lse_out;
 }
 
-template <int D>
-hipError_t launch_b128(const Geom& g, const void* Q, const int32_t* sel, int keep,
+template <int D, int BLK>
+hipError_t launch_rows(const Geom& g, const void* Q, const int32_t* sel, int keep,
                      const int32_t* slot_of, const void* Kp, const void* Vp, int64_t cap,
                      float scale, const AttnPart& part, void* O, bool out_bf16, float* lse,
                      hipStream_t s) {
@@ -807,12 +808,12 @@ hipError_t launch_b128(const Geom& g, const void* Q, const int32_t* sel, int kee
     const float c2 = scale * kLog2e;
     const size_t dyn = size_t(keep) * sizeof(int32_t);
     if (out_bf16)
-        attn_b128_kernel<D, true><<<G, 256, dyn, s>>>(
+        attn_rows_kernel<D, BLK, true><<<G, CfgRows<D, BLK>::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
             part.acc, 1, part.order);
     else
-        attn_b128_kernel<D, false><<<G, 256, dyn, s>>>(
+        attn_rows_kernel<D, BLK, false><<<G, CfgRows<D, BLK>::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
             part.acc, 1, part.order);
@@ -851,10 +852,10 @@ hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, in
                             bool out_bf16, float* lse, hipStream_t s) {
     (void)hipGetLastError();
     if (g.d == 128 && g.block == 128)
-        return launch_b128<128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
+        return launch_rows<128, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                               out_bf16, lse, s);
     if (g.d == 64 && g.block == 128)
-        return launch_b128<64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
+        return launch_rows<64, 128>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                              out_bf16, lse, s);
     if (g.d == 64 && g.block == 64)
         return launch_shape<64, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
