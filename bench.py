@@ -54,6 +54,9 @@ def parse_args(argv=None):
                     help="heads per chunk of a remote shard (shard-by-shard attention)")
     ap.add_argument("--tail-chunk-heads", type=int, default=2,
                     help="heads per chunk of the last remote shard")
+    ap.add_argument("--no-flush", action="store_true",
+                    help="do not overwrite a 512 MiB buffer between steps (it evicts the "
+                         "Infinity Cache and L2 so each step starts cold)")
     ap.add_argument("--extensions", action="store_true",
                     help="also measure shard-by-shard attention, CDF selection, routing and placement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -506,15 +509,26 @@ def main(argv=None) -> int:
                                     O=bufs["O"], lse=bufs["lse"], stream=stream)
         if ev: ev[4].record(stream)
 
+    # Between steps a 512 MiB buffer is overwritten on the same stream, so every
+    # step starts with the Infinity Cache (256 MB) and the L2s holding none of
+    # its inputs. The overwrite lies outside the stage events.
+    flush = None if a.no_flush else torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+
+    def cold():
+        if flush is not None:
+            flush.fill_(0x5A)
+
     for _ in range(a.warmup):
+        cold()
         step()
     torch.cuda.synchronize()
 
-    # Timed region: K steps back to back, per-stage HIP events on the same stream.
+    # Timed region: K steps, per-stage HIP events on the same stream.
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(a.steps)]
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     for s in range(a.steps):
+        cold()
         step(evs[s])
     torch.cuda.synchronize()
     wall_ms = (time.perf_counter() - t_wall) * 1e3 / a.steps
@@ -553,6 +567,7 @@ def main(argv=None) -> int:
         },
         "stages_ms": stage_ms,
         "wall_ms_per_step": wall_ms,
+        "cache_flushed_between_steps": flush is not None,
         "attention": {
             "algorithmic_tflop": flops / 1e12,
             "kernel_ms": stage_ms["block_sparse_attn"],
