@@ -253,14 +253,6 @@ __global__ __launch_bounds__(256) void gather_kernel(const int32_t* __restrict__
 // lanes, so every store instruction writes whole 128-byte row segments.
 constexpr int kStreamGrid = 512;
 
-__device__ __forceinline__ uint4 load_nt(const char* p) {
-    typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p)));
-}
-__device__ __forceinline__ void store_nt(char* p, uint4 v) {
-    typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-    __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
-}
 
 template <bool BF16, bool WHOLE>  // WHOLE: a K block is a multiple of 1,024 chunks
 __global__ __launch_bounds__(256) void gather_stream_kernel(

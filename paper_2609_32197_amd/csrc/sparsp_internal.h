@@ -124,4 +124,15 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float x) {
     return u >> 16;
 }
 
+// 16-byte global load and store with the non-temporal hint, for data that
+// streams through once (the caches keep less of it).
+__device__ __forceinline__ uint4 load_nt(const char* p) {
+    typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p)));
+}
+__device__ __forceinline__ void store_nt(char* p, uint4 v) {
+    typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(__builtin_bit_cast(u32x4_t, v), reinterpret_cast<u32x4_t*>(p));
+}
+
 }  // namespace sparsp
