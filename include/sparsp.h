@@ -203,56 +203,6 @@ int sparsp_block_sparse_attn_ordered(const sparsp_geom* g, const void* Q, const 
                                      int32_t out_dtype, float* lse, void* stream);
 
 /*
- * Bytes of device workspace that sparsp_block_sparse_attn_split needs to hold
- * up to max_pieces row pieces: the work items ((H*nq + max_pieces) x 16 B), the
- * split rows' first slots (H*nq x 4 B), and per piece a float32 partial output
- * (block x d x 4 B) and its lse (block x 4 B), each section 256-byte aligned.
- * Returns the size (>= 0), or a negative sparsp_status for a bad geometry or
- * max_pieces < 0. Host only.
- */
-int64_t sparsp_split_workspace_bytes(const sparsp_geom* g, int32_t max_pieces);
-
-/*
- * sparsp_block_sparse_attn with long rows split over several workgroups, for
- * selections whose rows keep very different numbers of blocks (CDF mode,
- * Section 8.1), where the longest row alone can outlast every other.
- *
- * Each split row is cut into pieces of at most T = min(piece_blocks, n) kept
- * blocks; each piece runs as its own workgroup and leaves its float32 partial
- * (O over its keys, normalised by their sum, and their log-sum-exp) in the
- * workspace; a final pass merges the pieces of each split row through the
- * log-sum-exp (the online-softmax merge of Section 2.3) into O and lse. Rows
- * that are not split are computed as in sparsp_block_sparse_attn.
- *   - counts: int32 [H, nq], the kept blocks of each local row (as written by
- *     sparsp_cdf_mask; clamped into [0, n]). It decides which rows split and
- *     how the pieces are balanced, not which blocks are attended: the pieces
- *     of a row partition [0, n) at its kept blocks number T, 2T, ..., so
- *     every kept block is used once whatever the counts say.
- *   - A row splits when its count exceeds T and is at least the smallest
- *     threshold whose split rows need no more than max_pieces pieces
- *     (ceil(count / T) each); max_pieces = 0 splits nothing.
- *   - Launch order: the layout of sparsp_row_order over work items (whole rows
- *     and pieces): heads on eight XCD queues by total count, each queue
- *     longest item first, queues interleaved.
- *   - workspace: device memory of at least
- *     sparsp_split_workspace_bytes(g, max_pieces) bytes, 16-byte aligned,
- *     caller-owned; its contents on entry do not matter and on return are
- *     unspecified. Calls that share a workspace must not overlap.
- * The launch has H*nq + max_pieces workgroups (unused ones exit at once).
- * Results equal sparsp_block_sparse_attn's up to the rounding of the merge
- * (float32). Errors: those of sparsp_block_sparse_attn; SPARSP_E_INVALID for
- * a NULL counts or workspace, piece_blocks < 1, max_pieces < 0, a workspace
- * smaller than required or misaligned, or H*nq + max_pieces above 2^31 - 1.
- */
-int sparsp_block_sparse_attn_split(const sparsp_geom* g, const void* Q, const int32_t* sel,
-                                   int32_t keep, const int32_t* counts, const int32_t* slot_of,
-                                   const void* K_packed, const void* V_packed,
-                                   int64_t capacity_blocks, float softmax_scale,
-                                   int32_t piece_blocks, int32_t max_pieces, void* workspace,
-                                   int64_t workspace_bytes, void* O, int32_t out_dtype,
-                                   float* lse, void* stream);
-
-/*
  * Shard-by-shard attention (Section 2.3: a rank attends to one owner's KV
  * shard at a time and folds the partial result in with the online softmax;
  * Section 7: shards are cut into chunks of heads and ordered to shorten the

@@ -11,8 +11,6 @@ a tensor is not on the GPU, the call raises.
     sparsp_demand_union_gather  per-head demand (Eq. 2) and packed K/V (Section 5.2)
     sparsp_block_sparse_attn    attention of the local query blocks (Eq. 1)
     sparsp_cdf_mask             CDF-mode block mask (Section 8.1), instead of top-k
-    sparsp_row_order            longest-first launch order for rows of unequal length
-    sparsp_block_sparse_attn_split  attention with long rows split over workgroups
 
 Shard-by-shard attention (Section 2.3, Section 7):
 
@@ -74,12 +72,6 @@ __all__ = [
     "sparsp_remote_demand",
     "sparsp_pack_for_consumers",
     "sparsp_route_volume",
-    "sparsp_row_order",
-    "sparsp_split_workspace_bytes",
-    "sparsp_block_sparse_attn_split",
-    "row_order",
-    "split_workspace_bytes",
-    "block_sparse_attn_split",
     "pack_for_consumers",
     "route_volume",
     "periodic_placement",
@@ -190,12 +182,7 @@ _SIGNATURES = {
     "sparsp_block_sparse_attn_ordered": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP, _VP,
                                          _VP, ctypes.c_int64, ctypes.c_float, _VP, _VP,
                                          ctypes.c_int32, _VP, _VP],
-    "sparsp_split_workspace_bytes": [ctypes.POINTER(_Geom), _I32],
-    "sparsp_block_sparse_attn_split": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP, _VP,
-                                       _VP, _VP, ctypes.c_int64, ctypes.c_float, _I32, _I32, _VP,
-                                       ctypes.c_int64, _VP, ctypes.c_int32, _VP, _VP],
 }
-_RESTYPES = {"sparsp_split_workspace_bytes": ctypes.c_int64}
 
 
 def load_library(path: Optional[str] = None) -> ctypes.CDLL:
@@ -211,7 +198,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         for name, args in _SIGNATURES.items():
             fn = getattr(lib, name)
             fn.argtypes = args
-            fn.restype = _RESTYPES.get(name, ctypes.c_int)
+            fn.restype = ctypes.c_int
         lib.sparsp_last_error.argtypes = []
         lib.sparsp_last_error.restype = ctypes.c_char_p
         lib.sparsp_version.argtypes = []
@@ -432,61 +419,6 @@ def sparsp_row_order(geom: Geometry, counts, order=None, stream=None):
                                            _dev(o, "order", torch.int32, (g.H * g.nq,)),
                                            _stream(stream, counts.device)))
     return o
-
-
-def sparsp_split_workspace_bytes(geom: Geometry, max_pieces: int) -> int:
-    """Bytes of workspace sparsp_block_sparse_attn_split needs for max_pieces pieces."""
-    gs = geom.c_struct()
-    nbytes = int(load_library().sparsp_split_workspace_bytes(ctypes.byref(gs), int(max_pieces)))
-    _check(nbytes if nbytes < 0 else 0)
-    return nbytes
-
-
-def sparsp_block_sparse_attn_split(geom: Geometry, Q, sel, slot_of, K_packed, V_packed, counts,
-                                   piece_blocks: int, max_pieces: int, workspace=None,
-                                   softmax_scale: Optional[float] = None,
-                                   out_dtype: Optional[int] = None, O=None, lse=None,
-                                   want_lse: bool = True, stream=None):
-    """Block-sparse attention with rows longer than piece_blocks kept blocks split
-    over several workgroups (at most max_pieces pieces in all) and merged.
-    counts: int32 [H, nq] kept blocks per row (from sparsp_cdf_mask). workspace:
-    a device tensor of at least sparsp_split_workspace_bytes(geom, max_pieces)
-    bytes, allocated here when None. Returns (O, lse or None)."""
-    torch = _torch()
-    g = geom
-    et = _elem_dtype(g)
-    keep = int(sel.shape[-1])
-    if out_dtype is None:
-        out_dtype = g.dtype
-    odt = torch.bfloat16 if out_dtype == BF16 else torch.float32
-    if softmax_scale is None:
-        softmax_scale = ctypes.c_float(1.0 / math.sqrt(g.d)).value
-    o = O if O is not None else _empty((g.H, g.nq * g.block, g.d), odt, Q)
-    ls = lse if lse is not None else (
-        _empty((g.H, g.nq * g.block), torch.float32, Q) if want_lse else None)
-    if K_packed.dim() != 3 or V_packed.dim() != 3:
-        raise ValueError("K_packed and V_packed must be 3-D")
-    cap = int(K_packed.shape[0])
-    if tuple(K_packed.shape[1:]) != (g.block, g.d) or tuple(V_packed.shape) != (cap, g.d, g.block):
-        raise ValueError("packed buffers must be [cap, block, d] and [cap, d, block]")
-    need = sparsp_split_workspace_bytes(g, max_pieces)
-    ws = workspace if workspace is not None else _empty((max(need, 1),), torch.uint8, Q)
-    if not ws.is_cuda or not ws.is_contiguous():
-        raise ValueError("workspace must be a contiguous cuda tensor")
-    ws_bytes = ws.numel() * ws.element_size()
-    gs = g.c_struct()
-    _check(load_library().sparsp_block_sparse_attn_split(
-        ctypes.byref(gs), _dev(Q, "Q", et, (g.H, g.L, g.d)),
-        _dev(sel, "sel", torch.int32, (g.H, g.nq, keep)), ctypes.c_int32(keep),
-        _dev(counts, "counts", torch.int32, (g.H, g.nq)),
-        _dev(slot_of, "slot_of", torch.int32, (g.H, g.n)), _dev(K_packed, "K_packed", et),
-        _dev(V_packed, "V_packed", et), ctypes.c_int64(cap), ctypes.c_float(softmax_scale),
-        ctypes.c_int32(int(piece_blocks)), ctypes.c_int32(int(max_pieces)), ws.data_ptr(),
-        ctypes.c_int64(ws_bytes), _dev(o, "O", odt, (g.H, g.nq * g.block, g.d)),
-        ctypes.c_int32(out_dtype),
-        _dev(ls, "lse", torch.float32, (g.H, g.nq * g.block)) if ls is not None else None,
-        _stream(stream, Q.device)))
-    return o, ls
 
 
 # ---------------------------------------------------------------------------
@@ -712,8 +644,6 @@ def sparsp_mfma_probe(iters: int, workgroups: int, sink, stream=None) -> None:
 
 block_scores = sparsp_block_scores
 row_order = sparsp_row_order
-split_workspace_bytes = sparsp_split_workspace_bytes
-block_sparse_attn_split = sparsp_block_sparse_attn_split
 topk_mask = sparsp_topk_mask
 demand_union_gather = sparsp_demand_union_gather
 block_sparse_attn = sparsp_block_sparse_attn

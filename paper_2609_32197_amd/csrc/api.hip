@@ -159,23 +159,6 @@ int attn_whole(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t 
     return hip_status(e, what);
 }
 
-// Workspace sections of sparsp_block_sparse_attn_split (byte offsets).
-struct SplitLayout {
-    int64_t items, piece_base, part_lse, part_o, total;
-};
-
-SplitLayout split_layout(const sparsp::Geom& G, int64_t pieces) {
-    auto up = [](int64_t x) { return (x + 255) / 256 * 256; };
-    const int64_t rows = int64_t(G.H) * G.nq;
-    SplitLayout l;
-    l.items = 0;
-    l.piece_base = up(l.items + (rows + pieces) * int64_t(sizeof(sparsp::SplitItem)));
-    l.part_lse = up(l.piece_base + rows * 4);
-    l.part_o = up(l.part_lse + pieces * G.block * 4);
-    l.total = up(l.part_o + pieces * G.block * int64_t(G.d) * 4);
-    return l;
-}
-
 }  // namespace
 
 extern "C" {
@@ -280,68 +263,6 @@ int sparsp_block_sparse_attn_ordered(const sparsp_geom* g, const void* Q, const 
     return attn_whole(g, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
                       softmax_scale, row_order, O, out_dtype, lse, stream,
                       "sparsp_block_sparse_attn_ordered");
-}
-
-int64_t sparsp_split_workspace_bytes(const sparsp_geom* g, int32_t max_pieces) {
-    sparsp::Geom G;
-    if (int rc = derive(g, &G)) return rc;
-    if (max_pieces < 0) return fail(SPARSP_E_INVALID, "max_pieces = %d < 0", max_pieces);
-    ok();
-    return split_layout(G, max_pieces).total;
-}
-
-int sparsp_block_sparse_attn_split(const sparsp_geom* g, const void* Q, const int32_t* sel,
-                                   int32_t keep, const int32_t* counts, const int32_t* slot_of,
-                                   const void* K_packed, const void* V_packed,
-                                   int64_t capacity_blocks, float softmax_scale,
-                                   int32_t piece_blocks, int32_t max_pieces, void* workspace,
-                                   int64_t workspace_bytes, void* O, int32_t out_dtype,
-                                   float* lse, void* stream) {
-    sparsp::Geom G;
-    if (int rc = derive(g, &G)) return rc;
-    if (!O || !counts || !workspace) return fail(SPARSP_E_INVALID, "NULL pointer");
-    if (int rc = check_attn(G, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
-                            softmax_scale))
-        return rc;
-    if (!aligned16(O) || !aligned16(workspace))
-        return fail(SPARSP_E_INVALID, "O and the workspace must be 16-byte aligned");
-    if (out_dtype != SPARSP_F32 && out_dtype != SPARSP_BF16)
-        return fail(SPARSP_E_DTYPE, "unknown out_dtype %d", out_dtype);
-    if (!G.bf16 && out_dtype != SPARSP_F32)
-        return fail(SPARSP_E_DTYPE, "f32 inputs produce f32 output only");
-    if (piece_blocks < 1) return fail(SPARSP_E_INVALID, "piece_blocks = %d < 1", piece_blocks);
-    if (max_pieces < 0) return fail(SPARSP_E_INVALID, "max_pieces = %d < 0", max_pieces);
-    const int64_t rows = int64_t(G.H) * G.nq;
-    if (rows + max_pieces > INT32_MAX)
-        return fail(SPARSP_E_INVALID, "H*nq + max_pieces exceeds 2^31 - 1");
-    const SplitLayout l = split_layout(G, max_pieces);
-    if (workspace_bytes < l.total)
-        return fail(SPARSP_E_INVALID, "workspace of %lld bytes, %lld needed",
-                    (long long)workspace_bytes, (long long)l.total);
-    char* ws = static_cast<char*>(workspace);
-    auto* items = reinterpret_cast<sparsp::SplitItem*>(ws + l.items);
-    auto* piece_base = reinterpret_cast<int32_t*>(ws + l.piece_base);
-    auto* part_lse = reinterpret_cast<float*>(ws + l.part_lse);
-    auto* part_o = reinterpret_cast<float*>(ws + l.part_o);
-    const int T = piece_blocks < G.n ? piece_blocks : G.n;
-    hipStream_t s = (hipStream_t)stream;
-    hipError_t e = sparsp::launch_split_plan(counts, sel, G.H, G.nq, G.n, keep, T, max_pieces,
-                                             items, piece_base, s);
-    if (e != hipSuccess) return hip_status(e, "sparsp_block_sparse_attn_split (plan)");
-    sparsp::AttnPart part{0, G.n, 0, G.H, 0};
-    part.items = items;
-    part.n_items = int(rows + max_pieces);
-    part.part_o = part_o;
-    part.part_lse = part_lse;
-    const bool out_bf16 = out_dtype == SPARSP_BF16;
-    e = G.bf16 ? sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed,
-                                          capacity_blocks, softmax_scale, part, O, out_bf16, lse, s)
-               : sparsp::launch_attn_f32(G, (const float*)Q, sel, keep, slot_of,
-                                         (const float*)K_packed, (const float*)V_packed,
-                                         capacity_blocks, softmax_scale, part, (float*)O, lse, s);
-    if (e != hipSuccess) return hip_status(e, "sparsp_block_sparse_attn_split (attention)");
-    e = sparsp::launch_split_merge(G, part_o, part_lse, piece_base, counts, T, O, out_bf16, lse, s);
-    return hip_status(e, "sparsp_block_sparse_attn_split (merge)");
 }
 
 int sparsp_row_order(const sparsp_geom* g, const int32_t* counts, int32_t* order, void* stream) {

@@ -201,8 +201,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                       float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
                       int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
                       int h_lo, int n_heads, int acc, int remap,
-                      const int32_t* __restrict__ order, const SplitItem* __restrict__ items,
-                      float* __restrict__ part_o, float* __restrict__ part_lse) {
+                      const int32_t* __restrict__ order) {
     using C = Cfg<D, BLK>;
     // [buffer][K tile | V tile]; reused for the final merge.
     __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][C::TILE];
@@ -217,15 +216,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     // Workgroup -> (head, local query block), XCD-contiguous when remap is on.
     const int G = n_heads * nq;
     int wg = blockIdx.x;
-    int piece = -1;  // workspace slot of this piece of a split row
-    if (items) {     // split launch: one row, or one piece of a row
-        const SplitItem it = items[blockIdx.x];
-        if (it.row < 0 || it.row >= G) return;
-        wg = it.row;
-        kv_lo = max(kv_lo, it.kv_lo);
-        kv_hi = min(kv_hi, it.kv_hi);
-        piece = it.slot;
-    } else if (order) {  // an explicit row order (e.g. longest first); no XCD remap
+    if (order) {  // an explicit row order (e.g. longest first); no XCD remap
         wg = order[blockIdx.x];
         if (wg < 0 || wg >= G) return;
     } else if (remap) {
@@ -442,24 +433,6 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     const float fa = w_a * inv, fb = w_b * inv;
     const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + qg * 32 + qi;
     float lse_out = live ? (m + __log2f(l_tot)) * kLn2 : -INFINITY;
-    if (piece >= 0) {  // a piece of a split row: float32 partial into the workspace
-        const int64_t prow = int64_t(piece) * BLK + qg * 32 + qi;
-#pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                float o4[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int rr = 4 * q4 + u;
-                    o4[u] = live ? oacc[dt][rr] * fa + mine[(dt * 16 + rr) * 64 + lane] * fb : 0.f;
-                }
-                *reinterpret_cast<float4*>(part_o + prow * D + 32 * dt + 8 * q4 + 4 * g) =
-                    make_float4(o4[0], o4[1], o4[2], o4[3]);
-            }
-        if (g == 0) part_lse[prow] = lse_out;
-        return;
-    }
     // Folding into a running result (O, lse, float32): with both log-sum-exps
     // in log2 units, the stored rows weigh ka and this part kb. Both lanes of
     // a row pair read the stored lse before the g == 0 lane rewrites it (the
@@ -553,8 +526,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                     float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
                     int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
                     int h_lo, int n_heads, int acc, int remap,
-                    const int32_t* __restrict__ order, const SplitItem* __restrict__ items,
-                    float* __restrict__ part_o, float* __restrict__ part_lse) {
+                    const int32_t* __restrict__ order) {
     using C = CfgRows<D, BLK>;
     __shared__ __attribute__((aligned(16))) uint16_t lk[C::TILE];
     __shared__ __attribute__((aligned(16))) uint16_t lv[C::TILE];
@@ -566,15 +538,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 
     const int G = n_heads * nq;
     int wg = blockIdx.x;
-    int piece = -1;  // workspace slot of this piece of a split row
-    if (items) {     // split launch: one row, or one piece of a row
-        const SplitItem it = items[blockIdx.x];
-        if (it.row < 0 || it.row >= G) return;
-        wg = it.row;
-        kv_lo = max(kv_lo, it.kv_lo);
-        kv_hi = min(kv_hi, it.kv_hi);
-        piece = it.slot;
-    } else if (order) {  // an explicit row order (e.g. longest first); no XCD remap
+    if (order) {  // an explicit row order (e.g. longest first); no XCD remap
         wg = order[blockIdx.x];
         if (wg < 0 || wg >= G) return;
     } else if (remap) {
@@ -787,22 +751,6 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     const float inv = live ? 1.0f / l_tot : 0.f;
     const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + 32 * wave + qi;
     float lse_out = live ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
-    if (piece >= 0) {  // a piece of a split row: float32 partial into the workspace
-        const int64_t prow = int64_t(piece) * BLK + 32 * wave + qi;
-#pragma unroll
-        for (int dt = 0; dt < C::DT; ++dt)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                float4 o;
-                o.x = live ? oacc[dt][4 * q4] * inv : 0.f;
-                o.y = live ? oacc[dt][4 * q4 + 1] * inv : 0.f;
-                o.z = live ? oacc[dt][4 * q4 + 2] * inv : 0.f;
-                o.w = live ? oacc[dt][4 * q4 + 3] * inv : 0.f;
-                *reinterpret_cast<float4*>(part_o + prow * D + 32 * dt + 8 * q4 + 4 * g) = o;
-            }
-        if (g == 0) part_lse[prow] = lse_out;
-        return;
-    }
     float ka = 0.f, kb = 1.f;
     bool store = true;
     if (!OUT_BF16 && acc) {
@@ -856,19 +804,19 @@ hipError_t launch_rows(const Geom& g, const void* Q, const int32_t* sel, int kee
                      float scale, const AttnPart& part, void* O, bool out_bf16, float* lse,
                      hipStream_t s) {
     const int n_heads = part.h_hi - part.h_lo;
-    const int G = part.items ? part.n_items : n_heads * g.nq;
+    const int G = n_heads * g.nq;
     const float c2 = scale * kLog2e;
     const size_t dyn = size_t(keep) * sizeof(int32_t);
     if (out_bf16)
         attn_rows_kernel<D, BLK, true><<<G, CfgRows<D, BLK>::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, 1, part.order, part.items, part.part_o, part.part_lse);
+            part.acc, 1, part.order);
     else
         attn_rows_kernel<D, BLK, false><<<G, CfgRows<D, BLK>::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, 1, part.order, part.items, part.part_o, part.part_lse);
+            part.acc, 1, part.order);
     return hipGetLastError();
 }
 
@@ -879,7 +827,7 @@ hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int ke
                         hipStream_t s) {
     using C = Cfg<D, BLK>;
     const int n_heads = part.h_hi - part.h_lo;
-    const int G = part.items ? part.n_items : n_heads * g.nq;
+    const int G = n_heads * g.nq;
     const float c2 = scale * kLog2e;
     const int remap = 1;
     const size_t dyn = size_t(keep) * sizeof(int32_t);
@@ -887,12 +835,12 @@ hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int ke
         attn_bf16_kernel<D, BLK, true><<<G, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, remap, part.order, part.items, part.part_o, part.part_lse);
+            part.acc, remap, part.order);
     else
         attn_bf16_kernel<D, BLK, false><<<G, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, remap, part.order, part.items, part.part_o, part.part_lse);
+            part.acc, remap, part.order);
     return hipGetLastError();
 }
 

@@ -20,21 +20,12 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     const float* __restrict__ Kp, const float* __restrict__ Vp, float* __restrict__ O,
     float* __restrict__ lse, int L, int n, int d, int block, int i0, int nq, int keep,
     int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi, int h_lo, int acc,
-    const int32_t* __restrict__ order, int rows, const SplitItem* __restrict__ items,
-    float* __restrict__ part_o, float* __restrict__ part_lse) {
+    const int32_t* __restrict__ order, int rows) {
     __shared__ float ks[kKeys][DMAX];
     __shared__ float vs[DMAX][kKeys];
 
     int wg = blockIdx.x;
-    int piece = -1;  // workspace slot of this piece of a split row
-    if (items) {     // split launch: one row, or one piece of a row
-        const SplitItem it = items[blockIdx.x];
-        if (it.row < 0 || it.row >= rows) return;
-        wg = it.row;
-        kv_lo = max(kv_lo, it.kv_lo);
-        kv_hi = min(kv_hi, it.kv_hi);
-        piece = it.slot;
-    } else if (order) {  // an explicit row order (e.g. longest first)
+    if (order) {  // an explicit row order (e.g. longest first)
         wg = order[blockIdx.x];
         if (wg < 0 || wg >= rows) return;
     }
@@ -102,14 +93,6 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(
     const bool live = qvalid && l > 0.f;
     const float inv = live ? 1.0f / l : 0.f;
     const int64_t orow = (int64_t(h) * nq + r) * block + tid;
-    if (piece >= 0) {  // a piece of a split row: partial result into the workspace
-        const int64_t prow = int64_t(piece) * block + tid;
-#pragma unroll
-        for (int c = 0; c < DMAX; ++c)
-            if (c < d) part_o[prow * d + c] = o[c] * inv;
-        part_lse[prow] = live ? (m + log2f(l)) * 0.6931471805599453f : -INFINITY;
-        return;
-    }
     if (acc) {
         // Fold into the stored result through the log-sum-exp (log2 units);
         // a row with no key in this part leaves it untouched.
@@ -143,17 +126,14 @@ hipError_t launch_attn_f32(const Geom& g, const float* Q, const int32_t* sel, in
     const int threads = ((g.block + 63) / 64) * 64;
     const float c2 = scale * 1.4426950408889634f;
     const int G = (part.h_hi - part.h_lo) * g.nq;
-    const int grid = part.items ? part.n_items : G;
     if (g.d <= 64)
-        attn_f32_kernel<64><<<grid, threads, 0, s>>>(
-            Q, sel, slot_of, Kp, Vp, O, lse, g.L, g.n, g.d, g.block, g.i0, g.nq, keep, capacity,
-            c2, part.kv_lo, part.kv_hi, part.h_lo, part.acc, part.order, G, part.items,
-            part.part_o, part.part_lse);
+        attn_f32_kernel<64><<<G, threads, 0, s>>>(Q, sel, slot_of, Kp, Vp, O, lse, g.L, g.n, g.d,
+                                                  g.block, g.i0, g.nq, keep, capacity, c2,
+                                                  part.kv_lo, part.kv_hi, part.h_lo, part.acc, part.order, G);
     else
-        attn_f32_kernel<128><<<grid, threads, 0, s>>>(
-            Q, sel, slot_of, Kp, Vp, O, lse, g.L, g.n, g.d, g.block, g.i0, g.nq, keep, capacity,
-            c2, part.kv_lo, part.kv_hi, part.h_lo, part.acc, part.order, G, part.items,
-            part.part_o, part.part_lse);
+        attn_f32_kernel<128><<<G, threads, 0, s>>>(Q, sel, slot_of, Kp, Vp, O, lse, g.L, g.n,
+                                                   g.d, g.block, g.i0, g.nq, keep, capacity, c2,
+                                                   part.kv_lo, part.kv_hi, part.h_lo, part.acc, part.order, G);
     return hipGetLastError();
 }
 

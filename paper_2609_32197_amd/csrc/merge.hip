@@ -66,75 +66,7 @@ __global__ __launch_bounds__(256) void fill_identity_kernel(float* __restrict__ 
     for (int64_t i = start; i < rows; i += stride) lse[i] = -INFINITY;
 }
 
-// The same merge over the pieces of a split row (attention with long rows
-// split over several workgroups): piece p of row r sits in workspace slot
-// piece_base[r] + p, as (O_p normalised by its own sum, lse_p), for np =
-// ceil(count / T) pieces. The pieces cover disjoint key sets whose union is
-// the row's, so with m = max_p lse_p and w_p = exp(lse_p - m):
-//   O = sum_p w_p O_p / sum_p w_p,   lse = m + log sum_p w_p.
-// One workgroup per row; rows that were not split (piece_base < 0) were
-// written by the attention kernel itself and are left alone.
-constexpr int kMaxMergeBlock = 256;
-
-template <bool OUT_BF16>
-__global__ __launch_bounds__(256) void split_merge_kernel(
-    const float* __restrict__ part_o, const float* __restrict__ part_lse,
-    const int32_t* __restrict__ piece_base, const int32_t* __restrict__ counts, int n, int T,
-    int block, int d, void* __restrict__ O, float* __restrict__ lse) {
-    __shared__ float m_s[kMaxMergeBlock], inv_s[kMaxMergeBlock];
-    const int r = blockIdx.x;
-    const int base = piece_base[r];
-    if (base < 0) return;
-    const int np = (min(max(counts[r], 0), n) + T - 1) / T;
-    for (int q = threadIdx.x; q < block; q += blockDim.x) {
-        float m = -INFINITY;
-        for (int p = 0; p < np; ++p) m = fmaxf(m, part_lse[int64_t(base + p) * block + q]);
-        float w = 0.f;
-        if (m != -INFINITY)
-            for (int p = 0; p < np; ++p) {
-                const float lp = part_lse[int64_t(base + p) * block + q];
-                w += lp == -INFINITY ? 0.f : __expf(lp - m);
-            }
-        m_s[q] = m;
-        inv_s[q] = w > 0.f ? 1.0f / w : 0.f;
-        if (lse) lse[int64_t(r) * block + q] = w > 0.f ? m + __logf(w) : -INFINITY;
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < block * d; e += blockDim.x) {
-        const int q = e / d, c = e % d;
-        const float m = m_s[q];
-        float acc = 0.f;
-        if (m != -INFINITY)
-            for (int p = 0; p < np; ++p) {
-                const int64_t prow = int64_t(base + p) * block + q;
-                const float lp = part_lse[prow];
-                if (lp != -INFINITY) acc += __expf(lp - m) * part_o[prow * d + c];
-            }
-        const float v = acc * inv_s[q];
-        const int64_t at = (int64_t(r) * block + q) * d + c;
-        if constexpr (OUT_BF16)
-            static_cast<uint16_t*>(O)[at] = uint16_t(f32_to_bf16_bits(v));
-        else
-            static_cast<float*>(O)[at] = v;
-    }
-}
-
 }  // namespace
-
-hipError_t launch_split_merge(const Geom& g, const float* part_o, const float* part_lse,
-                              const int32_t* piece_base, const int32_t* counts, int T, void* O,
-                              bool out_bf16, float* lse, hipStream_t s) {
-    (void)hipGetLastError();
-    if (g.block > kMaxMergeBlock) return hipErrorInvalidValue;
-    const int rows = g.H * g.nq;
-    if (out_bf16)
-        split_merge_kernel<true><<<rows, 256, 0, s>>>(part_o, part_lse, piece_base, counts, g.n, T,
-                                                      g.block, g.d, O, lse);
-    else
-        split_merge_kernel<false><<<rows, 256, 0, s>>>(part_o, part_lse, piece_base, counts, g.n,
-                                                       T, g.block, g.d, O, lse);
-    return hipGetLastError();
-}
 
 hipError_t launch_fill_identity(float* O, float* lse, int64_t rows, int d, hipStream_t s) {
     (void)hipGetLastError();

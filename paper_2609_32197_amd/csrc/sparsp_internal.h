@@ -46,25 +46,9 @@ hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void*
 // (O, lse) already hold a running result and the part is folded into it
 // through the log-sum-exp instead of overwriting it; rows without a kept key
 // in the part are left untouched.
-// One workgroup's share of an attention launch with long rows split: row
-// `row` (h * nq + local block), only the kept blocks inside [kv_lo, kv_hi).
-// slot < 0: the whole row, written to O and lse as usual; slot >= 0: one
-// piece of a split row, written as a float32 partial (O normalised by its own
-// sum, lse) to workspace slot `slot`. row < 0 marks an unused item.
-struct alignas(16) SplitItem {
-    int32_t row, kv_lo, kv_hi, slot;
-};
-
 struct AttnPart {
     int kv_lo, kv_hi, h_lo, h_hi, acc;
     const int32_t* order = nullptr;  // workgroup w takes row order[w] (longest first), if set
-    // Split launch (acc must be 0, all heads): workgroup w takes items[w];
-    // the grid has n_items workgroups. Partials go to part_o [slots, block, d]
-    // and part_lse [slots, block].
-    const SplitItem* items = nullptr;
-    int n_items = 0;
-    float* part_o = nullptr;
-    float* part_lse = nullptr;
 };
 
 // Packed K/V copies of n_vheads virtual heads (virtual head v reads head v % g.H).
@@ -123,16 +107,6 @@ hipError_t launch_mfma_probe(int64_t iters, int workgroups, float* sink, hipStre
 // Rows (h * nq + r) on eight XCD queues by head, each queue longest first, interleaved.
 hipError_t launch_row_order(const int32_t* counts, int H, int nq, int n, int32_t* order,
                             hipStream_t s);
-// Work items for attention with long rows split into pieces of at most T kept
-// blocks (at most P pieces in all), in the row order's queue layout; writes
-// items [H * nq + P] and piece_base [H * nq] (first slot of a split row, -1).
-hipError_t launch_split_plan(const int32_t* counts, const int32_t* sel, int H, int nq, int n,
-                             int keep, int T, int P, SplitItem* items, int32_t* piece_base,
-                             hipStream_t s);
-// Merges the pieces of every split row into O (bf16 or float32) and lse.
-hipError_t launch_split_merge(const Geom& g, const float* part_o, const float* part_lse,
-                              const int32_t* piece_base, const int32_t* counts, int T, void* O,
-                              bool out_bf16, float* lse, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // device helpers

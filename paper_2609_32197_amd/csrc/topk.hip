@@ -324,203 +324,6 @@ __global__ __launch_bounds__(1024) void row_order_kernel(const int32_t* __restri
     }
 }
 
-// Work items for attention with long rows split (CDF rows keep from one to
-// a few hundred blocks; the longest alone can outlast all the others). The
-// same single-workgroup layout as the row order above, over items instead of
-// rows:
-//   1. which rows split: a row splits when its count c exceeds T and is at
-//      least c*, the smallest threshold for which the split rows need at most
-//      P pieces in all (ceil(c / T) pieces each); rows of equal count all
-//      split or all stay whole;
-//   2. workspace slots: split rows take consecutive slots in row order
-//      (piece_base), one per piece;
-//   3. piece p of a split row covers the kept blocks in [b_p, b_{p+1}), with
-//      b_0 = 0, b_np = n and b_p the row's (p T)-th kept block (clamped to be
-//      non-decreasing), so the pieces partition the row whatever its order;
-//      with an ascending row each piece holds T kept blocks, the last the
-//      rest. Its length is min(T, c - p T);
-//   4. heads dealt to the eight XCD queues exactly as in the row order (by
-//      their total count), each queue's items sorted longest first, the
-//      queues interleaved round-robin over their item counts;
-//   5. positions past the last item get row -1.
-__global__ __launch_bounds__(1024) void split_plan_kernel(
-    const int32_t* __restrict__ counts, const int32_t* __restrict__ sel, int H, int nq, int n,
-    int keep, int T, int P, SplitItem* __restrict__ items, int32_t* __restrict__ piece_base) {
-    __shared__ int hist[kMaxBlocks + 1];
-    __shared__ int64_t part[1024];
-    __shared__ int64_t tot[kMaxHeads];
-    __shared__ int head_at[kMaxHeads];
-    __shared__ int queue_of[kMaxHeads];
-    __shared__ int qlen[kXcds];
-    __shared__ int cstar_s;
-    const int tid = threadIdx.x;
-    const int R = H * nq;
-    auto cnt_of = [&](int row) { return min(max(counts[row], 0), n); };
-    // Block-wide inclusive scan of part[]; returns this thread's exclusive prefix.
-    auto scan = [&]() -> int64_t {
-        __syncthreads();
-        for (int off = 1; off < 1024; off <<= 1) {
-            const int64_t v = tid >= off ? part[tid - off] : 0;
-            __syncthreads();
-            part[tid] += v;
-            __syncthreads();
-        }
-        return tid ? part[tid - 1] : 0;
-    };
-
-    // 1. histogram of the counts, then c* from the suffix sums of pieces.
-    for (int c = tid; c <= n; c += 1024) hist[c] = 0;
-    if (tid == 0) cstar_s = n + 1;
-    __syncthreads();
-    for (int r = tid; r < R; r += 1024) atomicAdd(&hist[cnt_of(r)], 1);
-    __syncthreads();
-    const int per = (n + 1 + 1023) / 1024;  // count values per thread, n downwards
-    {
-        int64_t local = 0;
-        for (int k = 0; k < per; ++k) {
-            const int c = n - (tid * per + k);
-            if (c > T) local += int64_t(hist[c]) * ((c + T - 1) / T);
-        }
-        part[tid] = local;
-        int64_t run = scan();  // pieces of the rows with a count above this thread's range
-        int best = n + 1;
-        for (int k = 0; k < per; ++k) {
-            const int c = n - (tid * per + k);
-            if (c > T) {
-                run += int64_t(hist[c]) * ((c + T - 1) / T);
-                if (run <= P) best = c;
-            }
-        }
-        atomicMin(&cstar_s, best);
-    }
-    __syncthreads();
-    const int cstar = cstar_s;
-    auto npieces = [&](int c) { return (c > T && c >= cstar) ? (c + T - 1) / T : 1; };
-
-    // 2. slots of the split rows, in row order.
-    const int rper = (R + 1023) / 1024;
-    {
-        int64_t local = 0;
-        for (int k = 0; k < rper; ++k) {
-            const int r = tid * rper + k;
-            if (r < R && npieces(cnt_of(r)) > 1) local += npieces(cnt_of(r));
-        }
-        __syncthreads();  // everyone is done reading part[] above
-        part[tid] = local;
-        int64_t run = scan();
-        for (int k = 0; k < rper; ++k) {
-            const int r = tid * rper + k;
-            if (r >= R) break;
-            const int np = npieces(cnt_of(r));
-            piece_base[r] = np > 1 ? int32_t(run) : -1;
-            if (np > 1) run += np;
-        }
-    }
-
-    // 4. heads to queues, as in the row order.
-    for (int h = tid; h < H; h += 1024) {
-        int64_t t = 0;
-        for (int r = 0; r < nq; ++r) t += cnt_of(h * nq + r);
-        tot[h] = t;
-    }
-    if (tid < kXcds) qlen[tid] = 0;
-    __syncthreads();
-    for (int h = tid; h < H; h += 1024) {
-        int k = 0;
-        for (int o = 0; o < H; ++o) k += (tot[o] > tot[h]) || (tot[o] == tot[h] && o < h);
-        head_at[k] = h;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int64_t load[kXcds];
-        int room[kXcds];
-        for (int x = 0; x < kXcds; ++x) {
-            load[x] = 0;
-            room[x] = H / kXcds + (x < H % kXcds ? 1 : 0);
-        }
-        for (int k = 0; k < H; ++k) {
-            const int h = head_at[k];
-            int best = -1;
-            for (int x = 0; x < kXcds; ++x)
-                if (room[x] > 0 && (best < 0 || load[x] < load[best])) best = x;
-            queue_of[h] = best;
-            load[best] += tot[h];
-            --room[best];
-        }
-    }
-    __syncthreads();
-    for (int r = tid; r < R; r += 1024) atomicAdd(&qlen[queue_of[r / nq]], npieces(cnt_of(r)));
-    __syncthreads();
-    int ql[kXcds];
-    int n_items = 0;
-#pragma unroll
-    for (int x = 0; x < kXcds; ++x) {
-        ql[x] = qlen[x];
-        n_items += ql[x];
-    }
-    // The kept block that opens piece q (q >= 1) of row r, clamped to [lo, n].
-    auto bound = [&](int r, int q, int lo) {
-        const int64_t e = int64_t(q) * T;
-        const int j = e < keep ? sel[int64_t(r) * keep + e] : n;
-        return min(max(j, lo), n);
-    };
-
-    for (int x = 0; x < kXcds; ++x) {
-        if (ql[x] == 0) continue;
-        for (int c = tid; c <= n; c += 1024) hist[c] = 0;
-        __syncthreads();
-        for (int r = tid; r < R; r += 1024) {
-            if (queue_of[r / nq] != x) continue;
-            const int c = cnt_of(r), np = npieces(c);
-            if (np == 1) atomicAdd(&hist[c], 1);
-            else
-                for (int p = 0; p < np; ++p) atomicAdd(&hist[min(T, c - p * T)], 1);
-        }
-        __syncthreads();
-        // exclusive scan over the lengths n, n-1, ..., 0
-        int64_t local = 0;
-        for (int k = 0; k < per; ++k) {
-            const int idx = tid * per + k;
-            if (idx <= n) local += hist[n - idx];
-        }
-        part[tid] = local;
-        int64_t run = scan();
-        for (int k = 0; k < per; ++k) {
-            const int idx = tid * per + k;
-            if (idx <= n) {
-                const int c = hist[n - idx];
-                hist[n - idx] = int(run);
-                run += c;
-            }
-        }
-        __syncthreads();
-        auto place = [&](int len, SplitItem it) {
-            const int k = atomicAdd(&hist[len], 1);  // entry k of queue x
-            int pos = 0;
-#pragma unroll
-            for (int y = 0; y < kXcds; ++y) pos += min(k, ql[y]) + (y < x && ql[y] > k ? 1 : 0);
-            items[pos] = it;
-        };
-        for (int r = tid; r < R; r += 1024) {
-            if (queue_of[r / nq] != x) continue;
-            const int c = cnt_of(r), np = npieces(c);
-            if (np == 1) {
-                place(c, SplitItem{r, 0, n, -1});
-                continue;
-            }
-            const int base = piece_base[r];
-            int lo = 0;
-            for (int p = 0; p < np; ++p) {
-                const int hi = p + 1 < np ? bound(r, p + 1, lo) : n;
-                place(min(T, c - p * T), SplitItem{r, lo, hi, base + p});
-                lo = hi;
-            }
-        }
-        __syncthreads();
-    }
-    for (int i = n_items + tid; i < R + P; i += 1024) items[i] = SplitItem{-1, 0, 0, -1};
-}
-
 }  // namespace
 
 hipError_t launch_cdf(const Geom& g, const float* scores, float tau, const GlobalSet& gs,
@@ -551,14 +354,6 @@ hipError_t launch_row_order(const int32_t* counts, int H, int nq, int n, int32_t
                             hipStream_t st) {
     (void)hipGetLastError();
     row_order_kernel<<<1, 1024, 0, st>>>(counts, H, nq, n, order);
-    return hipGetLastError();
-}
-
-hipError_t launch_split_plan(const int32_t* counts, const int32_t* sel, int H, int nq, int n,
-                             int keep, int T, int P, SplitItem* items, int32_t* piece_base,
-                             hipStream_t st) {
-    (void)hipGetLastError();
-    split_plan_kernel<<<1, 1024, 0, st>>>(counts, sel, H, nq, n, keep, T, P, items, piece_base);
     return hipGetLastError();
 }
 

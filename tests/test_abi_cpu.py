@@ -29,8 +29,7 @@ def lib():
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:int|int64_t|const char\*)\s+(sparsp_\w+)\s*\(", text,
-                                 re.M)))
+    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(sparsp_\w+)\s*\(", text, re.M)))
 
 
 def test_header_declares_the_four_steps():
@@ -354,43 +353,3 @@ def test_row_order_and_ordered_attention_rejected(lib):
     assert attn(None) == E_INVALID
     assert attn(P, keep=0) == E_INVALID
     assert attn(P, keep=9) == E_INVALID
-
-
-def test_split_workspace_size(lib):
-    """Items (rows + pieces) x 16 B, first slots rows x 4 B, then per piece a
-    float32 block x d partial and block lse values, each section 256-aligned."""
-    up = lambda x: (x + 255) // 256 * 256
-    for H, L, d, block, i0, i1, dt, pieces in [(2, 1024, 128, 128, 0, 8, sp.BF16, 0),
-                                               (3, 1000, 20, 64, 2, 16, sp.F32, 7),
-                                               (40, 75600, 128, 128, 0, 147, sp.BF16, 512)]:
-        g = geom(H=H, L=L, d=d, block=block, i0=i0, i1=i1, dtype=dt)
-        rows = H * (i1 - i0)
-        want = up(up(up(up((rows + pieces) * 16) + rows * 4) + pieces * block * 4)
-                  + pieces * block * d * 4)
-        assert lib.sparsp_split_workspace_bytes(ctypes.byref(g), pieces) == want
-        assert sp.sparsp_split_workspace_bytes(sp.Geometry(H, L, d, block, i0, i1, dt),
-                                               pieces) == want
-    g = geom()
-    assert lib.sparsp_split_workspace_bytes(ctypes.byref(g), -1) == E_INVALID
-    bad = geom(i0=3, i1=3)
-    assert lib.sparsp_split_workspace_bytes(ctypes.byref(bad), 4) == E_INVALID
-
-
-def test_split_attention_rejected(lib):
-    g = geom(H=2, L=1024, d=128, block=128, i0=0, i1=8, dtype=sp.BF16)
-    need = lib.sparsp_split_workspace_bytes(ctypes.byref(g), 8)
-
-    def call(counts=P, piece=4, pieces=8, ws=P, ws_bytes=need, keep=4, out=sp.BF16, O=P):
-        return lib.sparsp_block_sparse_attn_split(ctypes.byref(g), P, P, keep, counts, P, P, P, 16,
-                                                  0.1, piece, pieces, ws, ws_bytes, O, out, None,
-                                                  None)
-    assert call(counts=None) == E_INVALID
-    assert call(ws=None) == E_INVALID
-    assert call(O=None) == E_INVALID
-    assert call(ws=P + 8) == E_INVALID          # misaligned workspace
-    assert call(ws_bytes=need - 1) == E_INVALID  # too small
-    assert call(piece=0) == E_INVALID
-    assert call(pieces=-1) == E_INVALID
-    assert call(pieces=(1 << 31) - 1) == E_INVALID  # rows + pieces above 2^31 - 1
-    assert call(keep=0) == E_INVALID
-    assert call(out=7) == E_DTYPE
