@@ -227,66 +227,130 @@ hipError_t launch_cdf_s(const Geom& g, const float* scores, float tau, const Glo
 //   4. the queues interleaved: entry k of queue x goes to the position that a
 //      round-robin walk over the queues gives it, i.e. x + 8k while all
 //      queues are that long.
-// A count outside [0, n] is clamped into it.
+// A count outside [0, n] is clamped into it. The head totals are summed over
+// all rows at once (LDS atomics), and each queue's pass walks only the rows
+// of its own heads; up to kCountCache rows, the counts are read from memory
+// once and kept in LDS.
 constexpr int kXcds = 8;
+constexpr int kCountCache = 14336;  // rows whose counts are kept in LDS (16 bits each)
+static_assert(kMaxBlocks < 65536, "counts must fit 16 bits");
+
+// Exclusive prefix sum of v over a 1024-thread workgroup: a shuffle scan in
+// each wave, then one over the 16 wave totals (wave_sums: 16 ints of LDS).
+// Two barriers; every thread must call it.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wave_sums) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int t = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += t;
+    }
+    if (lane == 63) wave_sums[w] = incl;
+    __syncthreads();
+    if (w == 0) {
+        int t = lane < 16 ? wave_sums[lane] : 0;
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) {
+            const int u = __shfl_up(t, off, 64);
+            if (lane >= off) t += u;
+        }
+        if (lane < 16) wave_sums[lane] = t;
+    }
+    __syncthreads();
+    return (w ? wave_sums[w - 1] : 0) + incl - v;
+}
 
 __global__ __launch_bounds__(1024) void row_order_kernel(const int32_t* __restrict__ counts,
                                                          int H, int nq, int n,
                                                          int32_t* __restrict__ order) {
     __shared__ int start[kMaxBlocks + 1];
-    __shared__ int part[1024];
-    __shared__ int64_t tot[kMaxHeads];
-    __shared__ int rank_of[kMaxHeads];   // head -> rank by total
+    __shared__ int wave_sums[16];
+    __shared__ unsigned long long tot[kMaxHeads];
     __shared__ int head_at[kMaxHeads];   // rank -> head
-    __shared__ int queue_of[kMaxHeads];  // head -> XCD queue
-    __shared__ int qlen[kXcds];
+    __shared__ int q_heads[kMaxHeads];   // heads grouped by queue, in dealing order
+    __shared__ int q_first[kXcds + 1];   // queue x's heads: q_heads[q_first[x] .. q_first[x+1])
+    __shared__ uint16_t cnt_s[kCountCache];  // the clamped counts, when they fit
     const int tid = threadIdx.x;
     auto cnt_of = [&](int row) { return min(max(counts[row], 0), n); };
+    const int rows = H * nq;
+    const bool cached = rows <= kCountCache;
+    auto cnt_at = [&](int row) { return cached ? int(cnt_s[row]) : cnt_of(row); };
 
-    for (int h = tid; h < H; h += 1024) {
-        int64_t t = 0;
-        for (int r = 0; r < nq; ++r) t += cnt_of(h * nq + r);
-        tot[h] = t;
+    // 1. totals per head, heads ranked by total. With the counts in LDS a
+    // thread sums its head's rows there; otherwise all rows are added in
+    // parallel (LDS atomics).
+    for (int h = tid; h < H; h += 1024) tot[h] = 0;
+    if (cached)
+        for (int r = tid; r < rows; r += 1024) cnt_s[r] = uint16_t(cnt_of(r));
+    __syncthreads();
+    if (cached) {
+        for (int h = tid; h < H; h += 1024) {
+            unsigned long long t = 0;
+            for (int r = 0; r < nq; ++r) t += cnt_s[h * nq + r];
+            tot[h] = t;
+        }
+    } else {
+        for (int r = tid; r < rows; r += 1024) atomicAdd(&tot[r / nq], (unsigned long long)cnt_of(r));
     }
     __syncthreads();
     for (int h = tid; h < H; h += 1024) {
         int k = 0;
         for (int o = 0; o < H; ++o) k += (tot[o] > tot[h]) || (tot[o] == tot[h] && o < h);
-        rank_of[h] = k;
         head_at[k] = h;
     }
+    if (tid <= kXcds) {  // queue x holds H/8 heads, the first H mod 8 queues one more
+        int f = 0;
+        for (int x = 0; x < tid; ++x) f += H / kXcds + (x < H % kXcds ? 1 : 0);
+        q_first[tid] = f;
+    }
     __syncthreads();
-    if (tid == 0) {
-        int64_t load[kXcds];
-        int room[kXcds];
-        for (int x = 0; x < kXcds; ++x) {
-            load[x] = 0;
-            room[x] = H / kXcds + (x < H % kXcds ? 1 : 0);
-            qlen[x] = room[x] * nq;
-        }
+    // 2. heads dealt to the queues in rank order, each to the least loaded
+    // queue with room (the lowest such queue on a tie); each queue's heads are
+    // listed together. One wave: lane x < 8 holds queue x's load and room,
+    // and a shuffle argmin over lanes 0..7 picks the queue for each head.
+    if (tid < 64) {
+        const int lane = tid;
+        unsigned long long load = 0;
+        int room = lane < kXcds ? H / kXcds + (lane < H % kXcds ? 1 : 0) : 0;
+        int fill = lane < kXcds ? q_first[lane] : 0;
         for (int k = 0; k < H; ++k) {
             const int h = head_at[k];
-            int best = -1;
-            for (int x = 0; x < kXcds; ++x)
-                if (room[x] > 0 && (best < 0 || load[x] < load[best])) best = x;
-            queue_of[h] = best;
-            load[best] += tot[h];
-            --room[best];
+            const unsigned long long t = tot[h];
+            unsigned long long key = (lane < kXcds && room > 0) ? load : ~0ull;
+            int arg = lane;
+#pragma unroll
+            for (int off = 1; off < kXcds; off <<= 1) {
+                const uint32_t lo = __shfl_xor(uint32_t(key), off, 64);
+                const uint32_t hi = __shfl_xor(uint32_t(key >> 32), off, 64);
+                const int oa = __shfl_xor(arg, off, 64);
+                const unsigned long long ok = (uint64_t(hi) << 32) | lo;
+                if (ok < key || (ok == key && oa < arg)) {
+                    key = ok;
+                    arg = oa;
+                }
+            }
+            if (lane < kXcds && lane == arg) {
+                q_heads[fill++] = h;
+                load += t;
+                --room;
+            }
         }
     }
     __syncthreads();
     int ql[kXcds];
 #pragma unroll
-    for (int x = 0; x < kXcds; ++x) ql[x] = qlen[x];
+    for (int x = 0; x < kXcds; ++x) ql[x] = (q_first[x + 1] - q_first[x]) * nq;
 
-    const int rows = H * nq;
+    // 3. per queue: counting sort of its rows by count, largest first, and
+    // placement at the queue's round-robin positions
     const int per = (n + 1 + 1023) / 1024;
     for (int x = 0; x < kXcds; ++x) {
         if (ql[x] == 0) continue;
+        const int* qh = q_heads + q_first[x];
         for (int c = tid; c <= n; c += 1024) start[c] = 0;
         __syncthreads();
-        for (int r = tid; r < rows; r += 1024)
-            if (queue_of[r / nq] == x) atomicAdd(&start[cnt_of(r)], 1);
+        for (int i = tid; i < ql[x]; i += 1024) atomicAdd(&start[cnt_at(qh[i / nq] * nq + i % nq)], 1);
         __syncthreads();
         // exclusive scan over the count values n, n-1, ..., 0
         int local = 0;
@@ -294,15 +358,7 @@ __global__ __launch_bounds__(1024) void row_order_kernel(const int32_t* __restri
             const int idx = tid * per + k;
             if (idx <= n) local += start[n - idx];
         }
-        part[tid] = local;
-        __syncthreads();
-        for (int off = 1; off < 1024; off <<= 1) {
-            const int v = tid >= off ? part[tid - off] : 0;
-            __syncthreads();
-            part[tid] += v;
-            __syncthreads();
-        }
-        int run = tid ? part[tid - 1] : 0;
+        int run = block_exclusive_scan(local, wave_sums);
         for (int k = 0; k < per; ++k) {
             const int idx = tid * per + k;
             if (idx <= n) {
@@ -312,9 +368,9 @@ __global__ __launch_bounds__(1024) void row_order_kernel(const int32_t* __restri
             }
         }
         __syncthreads();
-        for (int r = tid; r < rows; r += 1024) {
-            if (queue_of[r / nq] != x) continue;
-            const int k = atomicAdd(&start[cnt_of(r)], 1);  // place in queue x
+        for (int i = tid; i < ql[x]; i += 1024) {
+            const int r = qh[i / nq] * nq + i % nq;
+            const int k = atomicAdd(&start[cnt_at(r)], 1);  // place in queue x
             int pos = 0;  // round-robin position of entry k of queue x
 #pragma unroll
             for (int y = 0; y < kXcds; ++y) pos += min(k, ql[y]) + (y < x && ql[y] > k ? 1 : 0);

@@ -39,7 +39,9 @@ def _queues(counts, n):
 
 @pytest.mark.parametrize("H,nq,n,lo,hi", [
     (1, 1, 1, 0, 2), (2, 7, 16, 0, 17), (3, 40, 591, 1, 592), (40, 147, 591, 1, 300),
-    (2, 300, 4096, 0, 4097), (5, 11, 64, -3, 70), (19, 9, 128, 1, 129)])
+    (2, 300, 4096, 0, 4097), (5, 11, 64, -3, 70), (19, 9, 128, 1, 129),
+    # more rows than the kernel keeps in LDS (14,336): counts read from memory
+    (24, 929, 929, 0, 930), (1024, 16, 64, 0, 65), (112, 128, 256, 0, 257)])
 def test_row_order_balances_heads_and_sorts_rows(gpu, H, nq, n, lo, hi):
     torch = P.torch()
     rng = np.random.default_rng(H * 1000 + nq)
