@@ -94,9 +94,15 @@ def load_inputs(wl, seed, cache_dir, make_qkv):
     return q, k, v
 
 
-def file_sha(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def code_sha(path):
+    """sha256[:16] of a HIP source with its comments and blank lines removed: the
+    counters stay valid across comment edits and are dropped on any code change."""
+    with open(path) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    lines = [line.rstrip() for line in text.splitlines() if line.strip()]
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()[:16]
 
 
 def read_traffic():
@@ -104,11 +110,11 @@ def read_traffic():
     if not os.path.exists(COUNTERS):
         return None, "no counter summary"
     text = open(COUNTERS).read()
-    m_sha = re.search(r"source sha256\[:16\]:\s*`?([0-9a-f]{16})", text)
+    m_sha = re.search(r"code sha256\[:16\][^`]*`([0-9a-f]{16})`", text)
     m_b = re.search(r"HBM bytes per launch \(calibrated\):\s*([0-9.eE+]+)", text)
     if not m_sha or not m_b:
         return None, "counter summary unreadable"
-    if m_sha.group(1) != file_sha(ATTN_SRC):
+    if m_sha.group(1) != code_sha(ATTN_SRC):
         return None, "kernel changed since the counters were taken"
     return float(m_b.group(1)), "ok"
 

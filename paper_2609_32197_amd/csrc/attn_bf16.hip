@@ -25,9 +25,10 @@
 // Data movement (both). The kept blocks' K tile ([BLK, D]) and transposed V
 // tile ([D, BLK]) are copied HBM -> LDS with direct-to-LDS buffer loads
 // (buffer_load_dwordx4 ... lds); each wave waits for its own copies before the
-// barrier that publishes them. Within a block, all MFMA operands of a phase
-// are read from LDS up front (K before the score MFMAs, V^T before the
-// softmax). LDS rows carry an XOR
+// barrier that publishes them. The split-key kernel reads all MFMA operands
+// of a phase from LDS up front (K before the score MFMAs, V^T before the
+// softmax); the rows kernel reads them one k step ahead of the MFMAs that use
+// them. LDS rows carry an XOR
 // swizzle of their 16-byte chunks (applied through the source addresses of the
 // copies) so the MFMA operand reads are bank-conflict free. Workgroup ids are
 // remapped so that each of the eight XCDs walks a contiguous range of (head,
