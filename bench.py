@@ -499,6 +499,10 @@ def main(argv=None) -> int:
     )
     out_dtype = sp.BF16 if wl.dtype == "bf16" else sp.F32
     stream = torch.cuda.current_stream()
+    # Workspace that lets the attention call split the rows of its last, partial
+    # round of workgroups (sparsp_block_sparse_attn_balanced); empty for float32.
+    ws_bytes = sp.sparsp_attn_workspace_bytes(g, wl.keep)
+    attn_ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda") if ws_bytes > 0 else None
 
     def step(ev=None):
         if ev: ev[0].record(stream)
@@ -512,7 +516,8 @@ def main(argv=None) -> int:
         if ev: ev[3].record(stream)
         sp.sparsp_block_sparse_attn(g, Q, bufs["sel"], packed["slot_of"], packed["K_packed"],
                                     packed["V_packed"], wl.softmax_scale, out_dtype=out_dtype,
-                                    O=bufs["O"], lse=bufs["lse"], stream=stream)
+                                    O=bufs["O"], lse=bufs["lse"], stream=stream,
+                                    workspace=attn_ws)
         if ev: ev[4].record(stream)
 
     # Between steps a 512 MiB buffer is overwritten on the same stream, so every
@@ -575,6 +580,8 @@ def main(argv=None) -> int:
         "wall_ms_per_step": wall_ms,
         "cache_flushed_between_steps": flush is not None,
         "attention": {
+            "call": "sparsp_block_sparse_attn_balanced" if attn_ws is not None
+                    else "sparsp_block_sparse_attn",
             "algorithmic_tflop": flops / 1e12,
             "kernel_ms": stage_ms["block_sparse_attn"],
             "tflops": attn_tflops,

@@ -168,6 +168,43 @@ int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t*
                              void* O, int32_t out_dtype, float* lse, void* stream);
 
 /*
+ * Bytes of device workspace that sparsp_block_sparse_attn_balanced can use for
+ * this geometry and keep on the current device: one float32 partial block
+ * (block x (d + 1) x 4 bytes) per workgroup the attention kernel keeps
+ * resident at once. 0 when no split applies (float32 inputs). Returns the size
+ * (>= 0) or a negative sparsp_status for a bad geometry or keep. Host only.
+ */
+int64_t sparsp_attn_workspace_bytes(const sparsp_geom* g, int32_t keep);
+
+/*
+ * sparsp_block_sparse_attn with a workspace that lets the last round of
+ * workgroups fill the GPU. The launch runs one workgroup per local row: R =
+ * H*nq rows on the P workgroups the device holds at once, so the last round
+ * has only S = R mod P rows and most of the GPU idles while they run. With a
+ * workspace, each of those S rows is split into k = min(4, P / S) workgroups,
+ * each over a consecutive part of the row's kept blocks. The pieces write
+ * float32 partials (O normalised by its own sum, and lse) to the workspace,
+ * and a second kernel merges each row's pieces through the log-sum-exp: the
+ * online-softmax merge of Section 2.3. k shrinks to fit workspace_bytes.
+ *   - Rows outside the last round are computed exactly as by
+ *     sparsp_block_sparse_attn, bit for bit; split rows differ from it by
+ *     float32 rounding only.
+ *   - workspace: caller-owned device memory, 16-byte aligned; contents on entry
+ *     do not matter and on return are unspecified. Calls that share a workspace
+ *     must not overlap. With workspace NULL or workspace_bytes too small for
+ *     k = 2, with S = 0, or with float32 inputs, the call is exactly
+ *     sparsp_block_sparse_attn.
+ * Errors: those of sparsp_block_sparse_attn; SPARSP_E_INVALID for a
+ * misaligned workspace or workspace_bytes < 0.
+ */
+int sparsp_block_sparse_attn_balanced(const sparsp_geom* g, const void* Q, const int32_t* sel,
+                                      int32_t keep, const int32_t* slot_of, const void* K_packed,
+                                      const void* V_packed, int64_t capacity_blocks,
+                                      float softmax_scale, void* workspace,
+                                      int64_t workspace_bytes, void* O, int32_t out_dtype,
+                                      float* lse, void* stream);
+
+/*
  * Longest-first row order, for selections whose rows keep different numbers of
  * blocks (CDF mode, Section 8.1): a row whose kept list is several times the
  * mean otherwise starts late and sets the attention time alone.

@@ -11,6 +11,7 @@ a tensor is not on the GPU, the call raises.
     sparsp_demand_union_gather  per-head demand (Eq. 2) and packed K/V (Section 5.2)
     sparsp_block_sparse_attn    attention of the local query blocks (Eq. 1)
     sparsp_cdf_mask             CDF-mode block mask (Section 8.1), instead of top-k
+    sparsp_block_sparse_attn(..., workspace=)  attention with the last round balanced
 
 Shard-by-shard attention (Section 2.3, Section 7):
 
@@ -72,6 +73,10 @@ __all__ = [
     "sparsp_remote_demand",
     "sparsp_pack_for_consumers",
     "sparsp_route_volume",
+    "sparsp_row_order",
+    "sparsp_attn_workspace_bytes",
+    "row_order",
+    "attn_workspace_bytes",
     "pack_for_consumers",
     "route_volume",
     "periodic_placement",
@@ -182,7 +187,12 @@ _SIGNATURES = {
     "sparsp_block_sparse_attn_ordered": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP, _VP,
                                          _VP, ctypes.c_int64, ctypes.c_float, _VP, _VP,
                                          ctypes.c_int32, _VP, _VP],
+    "sparsp_attn_workspace_bytes": [ctypes.POINTER(_Geom), _I32],
+    "sparsp_block_sparse_attn_balanced": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP,
+                                          _VP, _VP, ctypes.c_int64, ctypes.c_float, _VP,
+                                          ctypes.c_int64, _VP, ctypes.c_int32, _VP, _VP],
 }
+_RESTYPES = {"sparsp_attn_workspace_bytes": ctypes.c_int64}
 
 
 def load_library(path: Optional[str] = None) -> ctypes.CDLL:
@@ -198,7 +208,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         for name, args in _SIGNATURES.items():
             fn = getattr(lib, name)
             fn.argtypes = args
-            fn.restype = ctypes.c_int
+            fn.restype = _RESTYPES.get(name, ctypes.c_int)
         lib.sparsp_last_error.argtypes = []
         lib.sparsp_last_error.restype = ctypes.c_char_p
         lib.sparsp_version.argtypes = []
@@ -366,12 +376,15 @@ def sparsp_demand_union_gather(geom: Geometry, mask, K, V, capacity_blocks: Opti
 
 def sparsp_block_sparse_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed,
                              softmax_scale: Optional[float] = None, out_dtype: Optional[int] = None,
-                             O=None, lse=None, want_lse: bool = True, stream=None, row_order=None):
+                             O=None, lse=None, want_lse: bool = True, stream=None, row_order=None,
+                             workspace=None):
     """Block-sparse attention. Returns (O [H, nq*block, d], lse [H, nq*block] or None).
 
     With row_order (int32 [H*nq], e.g. from sparsp_row_order) the rows are
     launched in that order (sparsp_block_sparse_attn_ordered); the outputs are
-    the same bit for bit."""
+    the same bit for bit. With workspace (a device tensor, e.g. of
+    sparsp_attn_workspace_bytes(geom, keep) bytes) the rows of the last round
+    of workgroups are split to fill the GPU (sparsp_block_sparse_attn_balanced)."""
     torch = _torch()
     g = geom
     et = _elem_dtype(g)
@@ -399,13 +412,30 @@ def sparsp_block_sparse_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed
     )
     gs = g.c_struct()
     lib = load_library()
-    if row_order is None:
+    if row_order is not None and workspace is not None:
+        raise ValueError("row_order and workspace cannot be combined")
+    if workspace is not None:
+        if not workspace.is_cuda or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous cuda tensor")
+        _check(lib.sparsp_block_sparse_attn_balanced(
+            ctypes.byref(gs), *args[:8], workspace.data_ptr(),
+            ctypes.c_int64(workspace.numel() * workspace.element_size()), *args[8:],
+            _stream(stream, Q.device)))
+    elif row_order is None:
         _check(lib.sparsp_block_sparse_attn(ctypes.byref(gs), *args, _stream(stream, Q.device)))
     else:
         ro = _dev(row_order, "row_order", torch.int32, (g.H * g.nq,))
         _check(lib.sparsp_block_sparse_attn_ordered(ctypes.byref(gs), *args[:8], ro, *args[8:],
                                                     _stream(stream, Q.device)))
     return o, ls
+
+
+def sparsp_attn_workspace_bytes(geom: Geometry, keep: int) -> int:
+    """Workspace bytes sparsp_block_sparse_attn(..., workspace=) can use (0: none applies)."""
+    gs = geom.c_struct()
+    nbytes = int(load_library().sparsp_attn_workspace_bytes(ctypes.byref(gs), int(keep)))
+    _check(nbytes if nbytes < 0 else 0)
+    return nbytes
 
 
 def sparsp_row_order(geom: Geometry, counts, order=None, stream=None):
@@ -644,6 +674,7 @@ def sparsp_mfma_probe(iters: int, workgroups: int, sink, stream=None) -> None:
 
 block_scores = sparsp_block_scores
 row_order = sparsp_row_order
+attn_workspace_bytes = sparsp_attn_workspace_bytes
 topk_mask = sparsp_topk_mask
 demand_union_gather = sparsp_demand_union_gather
 block_sparse_attn = sparsp_block_sparse_attn

@@ -134,7 +134,8 @@ int check_part(const sparsp::Geom& G, int kv_lo, int kv_hi, int h_lo, int h_hi) 
 int attn_whole(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t keep,
                const int32_t* slot_of, const void* K_packed, const void* V_packed,
                int64_t capacity_blocks, float softmax_scale, const int32_t* order, void* O,
-               int32_t out_dtype, float* lse, void* stream, const char* what) {
+               int32_t out_dtype, float* lse, void* stream, const char* what,
+               void* workspace = nullptr, int64_t workspace_bytes = 0) {
     sparsp::Geom G;
     if (int rc = derive(g, &G)) return rc;
     if (!O) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
@@ -148,6 +149,11 @@ int attn_whole(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t 
         return fail(SPARSP_E_DTYPE, "f32 inputs produce f32 output only");
     sparsp::AttnPart whole{0, G.n, 0, G.H, 0};
     whole.order = order;
+    if (workspace && workspace_bytes > 0) {
+        if (!aligned16(workspace)) return fail(SPARSP_E_INVALID, "workspace must be 16-byte aligned");
+        whole.ws = workspace;
+        whole.ws_bytes = workspace_bytes;
+    }
     hipStream_t s = (hipStream_t)stream;
     hipError_t e =
         G.bf16 ? sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed,
@@ -252,6 +258,29 @@ int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t*
     return attn_whole(g, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
                       softmax_scale, nullptr, O, out_dtype, lse, stream,
                       "sparsp_block_sparse_attn");
+}
+
+int64_t sparsp_attn_workspace_bytes(const sparsp_geom* g, int32_t keep) {
+    sparsp::Geom G;
+    if (int rc = derive(g, &G)) return rc;
+    if (keep < 1 || keep > G.n)
+        return fail(SPARSP_E_INVALID, "keep = %d outside [1, n = %d]", keep, G.n);
+    ok();
+    if (!G.bf16) return 0;
+    const bool shape = (G.d == 64 || G.d == 128) && (G.block == 64 || G.block == 128);
+    return shape ? sparsp::attn_tail_workspace_bytes(G, keep) : 0;
+}
+
+int sparsp_block_sparse_attn_balanced(const sparsp_geom* g, const void* Q, const int32_t* sel,
+                                      int32_t keep, const int32_t* slot_of, const void* K_packed,
+                                      const void* V_packed, int64_t capacity_blocks,
+                                      float softmax_scale, void* workspace,
+                                      int64_t workspace_bytes, void* O, int32_t out_dtype,
+                                      float* lse, void* stream) {
+    if (workspace_bytes < 0) return fail(SPARSP_E_INVALID, "workspace_bytes < 0");
+    return attn_whole(g, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                      softmax_scale, nullptr, O, out_dtype, lse, stream,
+                      "sparsp_block_sparse_attn_balanced", workspace, workspace_bytes);
 }
 
 int sparsp_block_sparse_attn_ordered(const sparsp_geom* g, const void* Q, const int32_t* sel,

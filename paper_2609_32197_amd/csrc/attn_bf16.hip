@@ -92,6 +92,28 @@ __device__ __forceinline__ float pair_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// XCD-aware row of workgroup index w: consecutive workgroups go to the eight
+// XCDs in turn, so XCD x runs indices x, x+8, ...; they get the x-th
+// contiguous range of rows, where neighbouring query blocks share KV blocks in
+// that XCD's L2.
+__device__ __forceinline__ int xcd_row(int w, int G) {
+    const int xcd = w & 7, idx = w >> 3, per = G >> 3, rem = G & 7;
+    return xcd * per + min(xcd, rem) + idx;
+}
+
+// Tail split: the rows of the last, partial round of workgroups (indices
+// tail_first .. G-1) run as tail_k workgroups each, so that round fills the
+// GPU. Workgroup tail_first + t*tail_k + p is piece p of tail row t, which
+// has index tail_first + t; index is the row index a workgroup works on.
+struct TailPiece {
+    int index, piece;
+};
+__device__ __forceinline__ TailPiece tail_piece(int w, int tail_first, int tail_k) {
+    if (tail_k > 1 && w >= tail_first)
+        return {tail_first + (w - tail_first) / tail_k, (w - tail_first) % tail_k};
+    return {w, -1};
+}
+
 template <int D, int BLK>
 struct Cfg {
     static constexpr int NQG = BLK / 32;          // query groups of 32
@@ -202,7 +224,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                       float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
                       int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
                       int h_lo, int n_heads, int acc, int remap,
-                      const int32_t* __restrict__ order) {
+                      const int32_t* __restrict__ order, int tail_first, int tail_k,
+                      float* __restrict__ part_o, float* __restrict__ part_lse) {
     using C = Cfg<D, BLK>;
     // [buffer][K tile | V tile]; reused for the final merge.
     __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][C::TILE];
@@ -217,12 +240,14 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     // Workgroup -> (head, local query block), XCD-contiguous when remap is on.
     const int G = n_heads * nq;
     int wg = blockIdx.x;
+    const TailPiece tp = tail_piece(wg, tail_first, tail_k);
     if (order) {  // an explicit row order (e.g. longest first); no XCD remap
         wg = order[blockIdx.x];
         if (wg < 0 || wg >= G) return;
     } else if (remap) {
-        const int xcd = wg & 7, idx = wg >> 3, per = G >> 3, rem = G & 7;
-        wg = xcd * per + min(xcd, rem) + idx;
+        wg = xcd_row(tp.index, G);
+    } else {
+        wg = tp.index;
     }
     const int h = h_lo + wg / nq, r = wg % nq;
     const int qtok = (i0 + r) * BLK + qg * 32 + qi;
@@ -289,10 +314,16 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     }
     // Folding into a running result: nothing to add when no block is kept here.
     if (acc && nkeep == 0) return;
+    const int32_t* kept = codes;  // this workgroup's kept list
+    if (tp.piece >= 0) {          // its share of a split tail row
+        const int e0 = tp.piece * nkeep / tail_k, e1 = (tp.piece + 1) * nkeep / tail_k;
+        kept = codes + e0;
+        nkeep = e1 - e0;
+    }
     // (the last compaction round ended with a barrier: codes are visible)
-    int code = nkeep > 0 ? codes[0] : -1;
+    int code = nkeep > 0 ? kept[0] : -1;
     if (nkeep > 0) issue(code, 0);
-    int next_code = nkeep > 1 ? codes[1] : -1;
+    int next_code = nkeep > 1 ? kept[1] : -1;
 
     floatx16 oacc[C::DT];
 #pragma unroll
@@ -313,7 +344,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         if (jj + 1 < nkeep) {
             issue(next_code, buf ^ 1);
             code = next_code;
-            next_code = (jj + 2 < nkeep) ? codes[jj + 2] : -1;
+            next_code = (jj + 2 < nkeep) ? kept[jj + 2] : -1;
         }
         if (cur < 0) continue;
 
@@ -434,6 +465,24 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     const float fa = w_a * inv, fb = w_b * inv;
     const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + qg * 32 + qi;
     float lse_out = live ? (m + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (tp.piece >= 0) {  // a piece of a split tail row: float32 partial into the workspace
+        const int64_t prow = int64_t(blockIdx.x - tail_first) * BLK + qg * 32 + qi;
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                float o4[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int rr = 4 * q4 + u;
+                    o4[u] = live ? oacc[dt][rr] * fa + mine[(dt * 16 + rr) * 64 + lane] * fb : 0.f;
+                }
+                *reinterpret_cast<float4*>(part_o + prow * D + 32 * dt + 8 * q4 + 4 * g) =
+                    make_float4(o4[0], o4[1], o4[2], o4[3]);
+            }
+        if (g == 0) part_lse[prow] = lse_out;
+        return;
+    }
     // Folding into a running result (O, lse, float32): with both log-sum-exps
     // in log2 units, the stored rows weigh ka and this part kb. Both lanes of
     // a row pair read the stored lse before the g == 0 lane rewrites it (the
@@ -527,7 +576,8 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                     float* __restrict__ lse, int L, int n, int i0, int nq, int keep,
                     int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
                     int h_lo, int n_heads, int acc, int remap,
-                    const int32_t* __restrict__ order) {
+                    const int32_t* __restrict__ order, int tail_first, int tail_k,
+                    float* __restrict__ part_o, float* __restrict__ part_lse) {
     using C = CfgRows<D, BLK>;
     __shared__ __attribute__((aligned(16))) uint16_t lk[C::TILE];
     __shared__ __attribute__((aligned(16))) uint16_t lv[C::TILE];
@@ -539,12 +589,14 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 
     const int G = n_heads * nq;
     int wg = blockIdx.x;
+    const TailPiece tp = tail_piece(wg, tail_first, tail_k);
     if (order) {  // an explicit row order (e.g. longest first); no XCD remap
         wg = order[blockIdx.x];
         if (wg < 0 || wg >= G) return;
     } else if (remap) {
-        const int xcd = wg & 7, idx = wg >> 3, per = G >> 3, rem = G & 7;
-        wg = xcd * per + min(xcd, rem) + idx;
+        wg = xcd_row(tp.index, G);
+    } else {
+        wg = tp.index;
     }
     const int h = h_lo + wg / nq, r = wg % nq;
     const int qtok = (i0 + r) * BLK + 32 * wave + qi;
@@ -584,6 +636,12 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         }
     }
     if (acc && nkeep == 0) return;
+    const int32_t* kept = codes;  // this workgroup's kept list
+    if (tp.piece >= 0) {          // its share of a split tail row
+        const int e0 = tp.piece * nkeep / tail_k, e1 = (tp.piece + 1) * nkeep / tail_k;
+        kept = codes + e0;
+        nkeep = e1 - e0;
+    }
 
     int kvoff[C::DMA], vvoff[C::DMA];
 #pragma unroll
@@ -612,8 +670,8 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     // waited for here, and the copies are issued behind its back (copy_tile).
     wait_vmem_all();
     if (nkeep > 0) {
-        copy_k(codes[0]);
-        copy_v(codes[0]);
+        copy_k(kept[0]);
+        copy_v(kept[0]);
     }
 
     floatx16 oacc[C::DT];
@@ -628,7 +686,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         __syncthreads();
     }
     for (int jj = 0; jj < nkeep; ++jj) {
-        const int cur = codes[jj];
+        const int cur = kept[jj];
         // Scores: S^T for the wave's 32 queries over all 128 keys of the block;
         // s[mt][rr] is key 32 mt + 16 (rr/8) + 8 g + rr%8.
         // k step outermost, so the four accumulators advance together and no
@@ -664,7 +722,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         __builtin_amdgcn_sched_barrier(0);
         wait_vmem_all();   // V(jj) landed
         __syncthreads();   // V(jj) visible; every wave is done with K(jj)
-        if (jj + 1 < nkeep) copy_k(codes[jj + 1]);
+        if (jj + 1 < nkeep) copy_k(kept[jj + 1]);
 
         // Softmax and output product at raised priority: where the other wave
         // on the SIMD is in its score MFMAs, this wave's VALU work issues first
@@ -744,7 +802,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 
         wait_vmem_all();   // K(jj+1) landed
         __syncthreads();   // K(jj+1) visible; every wave is done with V(jj)
-        if (jj + 1 < nkeep) copy_v(codes[jj + 1]);
+        if (jj + 1 < nkeep) copy_v(kept[jj + 1]);
     }
 
     const float l_tot = pair_sum(l_run);
@@ -752,6 +810,22 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     const float inv = live ? 1.0f / l_tot : 0.f;
     const int64_t orow = int64_t(h) * nq * BLK + int64_t(r) * BLK + 32 * wave + qi;
     float lse_out = live ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    if (tp.piece >= 0) {  // a piece of a split tail row: float32 partial into the workspace
+        const int64_t prow = int64_t(blockIdx.x - tail_first) * BLK + 32 * wave + qi;
+#pragma unroll
+        for (int dt = 0; dt < C::DT; ++dt)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                float4 o;
+                o.x = live ? oacc[dt][4 * q4] * inv : 0.f;
+                o.y = live ? oacc[dt][4 * q4 + 1] * inv : 0.f;
+                o.z = live ? oacc[dt][4 * q4 + 2] * inv : 0.f;
+                o.w = live ? oacc[dt][4 * q4 + 3] * inv : 0.f;
+                *reinterpret_cast<float4*>(part_o + prow * D + 32 * dt + 8 * q4 + 4 * g) = o;
+            }
+        if (g == 0) part_lse[prow] = lse_out;
+        return;
+    }
     float ka = 0.f, kb = 1.f;
     bool store = true;
     if (!OUT_BF16 && acc) {
@@ -799,6 +873,108 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     if (lse && g == 0 && store) lse[orow] = lse_out;
 }
 
+// Merge of the pieces of the split tail rows. Piece p of tail row t sits in
+// workspace slot t * tail_k + p as (O_p normalised by its own sum, lse_p in
+// natural log); the pieces cover disjoint parts of the row's kept blocks, so
+// with m = max_p lse_p and w_p = exp(lse_p - m)
+//   O = sum_p w_p O_p / sum_p w_p,   lse = m + log sum_p w_p
+// (the online-softmax merge of Section 2.3). One workgroup per tail row;
+// rows whose pieces are all empty (padded queries) get O = 0, lse = -inf.
+template <int D, int BLK, bool OUT_BF16>
+__global__ __launch_bounds__(256) void tail_merge_kernel(
+    const float* __restrict__ part_o, const float* __restrict__ part_lse, void* __restrict__ O,
+    float* __restrict__ lse, int G, int nq, int h_lo, int tail_first, int tail_k) {
+    const int t = blockIdx.x;
+    const int row = xcd_row(tail_first + t, G);
+    const int h = h_lo + row / nq, r = row % nq;
+    const int64_t orow0 = (int64_t(h) * nq + r) * BLK;
+    constexpr int C4 = D / 4;
+    for (int e = threadIdx.x; e < BLK * C4; e += blockDim.x) {
+        const int q = e / C4, c4 = e % C4;
+        float m = -INFINITY;
+        for (int p = 0; p < tail_k; ++p)
+            m = fmaxf(m, part_lse[(int64_t(t) * tail_k + p) * BLK + q]);
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        float wsum = 0.f;
+        if (m != -INFINITY)
+            for (int p = 0; p < tail_k; ++p) {
+                const int64_t prow = (int64_t(t) * tail_k + p) * BLK + q;
+                const float lp = part_lse[prow];
+                if (lp == -INFINITY) continue;
+                const float w = expf(lp - m);
+                const float4 x = reinterpret_cast<const float4*>(part_o + prow * D)[c4];
+                wsum += w;
+                acc.x += w * x.x;
+                acc.y += w * x.y;
+                acc.z += w * x.z;
+                acc.w += w * x.w;
+            }
+        const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
+        const int64_t at = (orow0 + q) * D + 4 * c4;
+        if constexpr (OUT_BF16) {
+            uint2 wv;
+            wv.x = f32_to_bf16_bits(acc.x * inv) | (f32_to_bf16_bits(acc.y * inv) << 16);
+            wv.y = f32_to_bf16_bits(acc.z * inv) | (f32_to_bf16_bits(acc.w * inv) << 16);
+            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(O) + at) = wv;
+        } else {
+            *reinterpret_cast<float4*>(static_cast<float*>(O) + at) =
+                make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+        }
+        if (c4 == 0 && lse) lse[orow0 + q] = wsum > 0.f ? m + logf(wsum) : -INFINITY;
+    }
+}
+
+constexpr int kMaxTailSplit = 4;
+
+// Workgroups of `kernel` that are resident at once on the current device.
+template <typename Kernel>
+int resident_slots(Kernel kernel, int threads, size_t dyn) {
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, dyn) != hipSuccess)
+        return 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    return per_cu * cus;
+}
+
+// The tail split of a launch of G rows on `slots` resident workgroups: the S
+// = G mod slots rows of the last, partial round run as k pieces each, k as
+// large as the round's free slots, kMaxTailSplit and the workspace allow.
+struct TailPlan {
+    int first, k;
+};
+TailPlan plan_tail(int G, int slots, int64_t piece_bytes, int64_t ws_bytes) {
+    if (slots <= 0) return {G, 1};
+    const int S = G % slots;
+    if (S == 0) return {G, 1};
+    int k = min(kMaxTailSplit, slots / S);
+    while (k > 1 && int64_t(S) * k * piece_bytes > ws_bytes) --k;
+    if (k < 2) return {G, 1};
+    return {G - S, k};
+}
+
+template <int D, int BLK, bool OUT>
+hipError_t launch_tail_merge(const Geom& g, const AttnPart& part, const TailPlan& tp, int G,
+                             const float* part_o, const float* part_lse, void* O, float* lse,
+                             hipStream_t s) {
+    const int S = G - tp.first;
+    tail_merge_kernel<D, BLK, OUT><<<S, 256, 0, s>>>(part_o, part_lse, O, lse, G, g.nq, part.h_lo,
+                                                     tp.first, tp.k);
+    return hipGetLastError();
+}
+
+// Workspace layout of a tail split: the partial outputs, then their lse.
+struct TailSpace {
+    float* part_o;
+    float* part_lse;
+};
+TailSpace tail_space(void* ws, const TailPlan& tp, int G, int D, int BLK) {
+    const int64_t pieces = int64_t(G - tp.first) * tp.k;
+    float* o = static_cast<float*>(ws);
+    return {o, o + pieces * BLK * D};
+}
+
 template <int D, int BLK>
 hipError_t launch_rows(const Geom& g, const void* Q, const int32_t* sel, int keep,
                      const int32_t* slot_of, const void* Kp, const void* Vp, int64_t cap,
@@ -808,17 +984,27 @@ hipError_t launch_rows(const Geom& g, const void* Q, const int32_t* sel, int kee
     const int G = n_heads * g.nq;
     const float c2 = scale * kLog2e;
     const size_t dyn = size_t(keep) * sizeof(int32_t);
+    constexpr int THREADS = CfgRows<D, BLK>::THREADS;
+    TailPlan tp{G, 1};
+    if (part.ws && !part.order && !part.acc)
+        tp = plan_tail(G, resident_slots(attn_rows_kernel<D, BLK, true>, THREADS, dyn),
+                       int64_t(BLK) * (D + 1) * 4, part.ws_bytes);
+    const TailSpace ts = tp.k > 1 ? tail_space(part.ws, tp, G, D, BLK) : TailSpace{nullptr, nullptr};
+    const int grid = tp.first + (G - tp.first) * tp.k;
     if (out_bf16)
-        attn_rows_kernel<D, BLK, true><<<G, CfgRows<D, BLK>::THREADS, dyn, s>>>(
+        attn_rows_kernel<D, BLK, true><<<grid, THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, 1, part.order);
+            part.acc, 1, part.order, tp.first, tp.k, ts.part_o, ts.part_lse);
     else
-        attn_rows_kernel<D, BLK, false><<<G, CfgRows<D, BLK>::THREADS, dyn, s>>>(
+        attn_rows_kernel<D, BLK, false><<<grid, THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, 1, part.order);
-    return hipGetLastError();
+            part.acc, 1, part.order, tp.first, tp.k, ts.part_o, ts.part_lse);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || tp.k < 2) return e;
+    return out_bf16 ? launch_tail_merge<D, BLK, true>(g, part, tp, G, ts.part_o, ts.part_lse, O, lse, s)
+                    : launch_tail_merge<D, BLK, false>(g, part, tp, G, ts.part_o, ts.part_lse, O, lse, s);
 }
 
 template <int D, int BLK>
@@ -832,17 +1018,26 @@ hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int ke
     const float c2 = scale * kLog2e;
     const int remap = 1;
     const size_t dyn = size_t(keep) * sizeof(int32_t);
+    TailPlan tp{G, 1};
+    if (part.ws && !part.order && !part.acc)
+        tp = plan_tail(G, resident_slots(attn_bf16_kernel<D, BLK, true>, C::THREADS, dyn),
+                       int64_t(BLK) * (D + 1) * 4, part.ws_bytes);
+    const TailSpace ts = tp.k > 1 ? tail_space(part.ws, tp, G, D, BLK) : TailSpace{nullptr, nullptr};
+    const int grid = tp.first + (G - tp.first) * tp.k;
     if (out_bf16)
-        attn_bf16_kernel<D, BLK, true><<<G, C::THREADS, dyn, s>>>(
+        attn_bf16_kernel<D, BLK, true><<<grid, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, remap, part.order);
+            part.acc, remap, part.order, tp.first, tp.k, ts.part_o, ts.part_lse);
     else
-        attn_bf16_kernel<D, BLK, false><<<G, C::THREADS, dyn, s>>>(
+        attn_bf16_kernel<D, BLK, false><<<grid, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, remap, part.order);
-    return hipGetLastError();
+            part.acc, remap, part.order, tp.first, tp.k, ts.part_o, ts.part_lse);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || tp.k < 2) return e;
+    return out_bf16 ? launch_tail_merge<D, BLK, true>(g, part, tp, G, ts.part_o, ts.part_lse, O, lse, s)
+                    : launch_tail_merge<D, BLK, false>(g, part, tp, G, ts.part_o, ts.part_lse, O, lse, s);
 }
 
 }  // namespace
@@ -865,6 +1060,22 @@ hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, in
         return launch_shape<128, 64>(g, Q, sel, keep, slot_of, Kp, Vp, capacity, scale, part, O,
                                      out_bf16, lse, s);
     return hipErrorInvalidValue;
+}
+
+int64_t attn_tail_workspace_bytes(const Geom& g, int keep) {
+    const size_t dyn = size_t(keep) * sizeof(int32_t);
+    int slots = 0;
+    if (g.d == 128 && g.block == 128)
+        slots = resident_slots(attn_rows_kernel<128, 128, true>, CfgRows<128, 128>::THREADS, dyn);
+    else if (g.d == 64 && g.block == 128)
+        slots = resident_slots(attn_rows_kernel<64, 128, true>, CfgRows<64, 128>::THREADS, dyn);
+    else if (g.d == 64 && g.block == 64)
+        slots = resident_slots(attn_bf16_kernel<64, 64, true>, Cfg<64, 64>::THREADS, dyn);
+    else if (g.d == 128 && g.block == 64)
+        slots = resident_slots(attn_bf16_kernel<128, 64, true>, Cfg<128, 64>::THREADS, dyn);
+    if (slots <= 0) return 0;
+    // the tail pieces never outnumber the resident slots
+    return int64_t(slots) * g.block * (g.d + 1) * 4;
 }
 
 }  // namespace sparsp

@@ -49,6 +49,11 @@ hipError_t launch_demand_gather(const Geom& g, const uint64_t* mask, const void*
 struct AttnPart {
     int kv_lo, kv_hi, h_lo, h_hi, acc;
     const int32_t* order = nullptr;  // workgroup w takes row order[w] (longest first), if set
+    // Workspace for the tail split of the bf16 kernels (whole launches only):
+    // the rows of the last, partial round of workgroups are split into pieces
+    // whose float32 partials go here and are merged by a second kernel.
+    void* ws = nullptr;
+    int64_t ws_bytes = 0;
 };
 
 // Packed K/V copies of n_vheads virtual heads (virtual head v reads head v % g.H).
@@ -70,6 +75,10 @@ hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, in
                             const int32_t* slot_of, const void* Kp, const void* Vp,
                             int64_t capacity, float scale, const AttnPart& part, void* O,
                             bool out_bf16, float* lse, hipStream_t s);
+
+// Bytes of workspace the tail split of a bf16 attention launch can use (0
+// when it does not apply): one float32 partial block per resident slot.
+int64_t attn_tail_workspace_bytes(const Geom& g, int keep);
 
 hipError_t launch_attn_f32(const Geom& g, const float* Q, const int32_t* sel, int keep,
                            const int32_t* slot_of, const float* Kp, const float* Vp,

@@ -29,7 +29,8 @@ def lib():
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:int|const char\*)\s+(sparsp_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:int|int64_t|const char\*)\s+(sparsp_\w+)\s*\(", text,
+                                 re.M)))
 
 
 def test_header_declares_the_four_steps():
@@ -353,3 +354,21 @@ def test_row_order_and_ordered_attention_rejected(lib):
     assert attn(None) == E_INVALID
     assert attn(P, keep=0) == E_INVALID
     assert attn(P, keep=9) == E_INVALID
+
+
+def test_balanced_attention_rejected(lib):
+    g = geom(H=2, L=1024, d=128, block=128, i0=0, i1=8, dtype=sp.BF16)
+
+    def call(ws=P, ws_bytes=1 << 20, keep=4, out=sp.BF16):
+        return lib.sparsp_block_sparse_attn_balanced(ctypes.byref(g), P, P, keep, P, P, P, 16, 0.1,
+                                                     ws, ws_bytes, P, out, None, None)
+    assert call(ws=P + 8) == E_INVALID        # misaligned workspace
+    assert call(ws_bytes=-1) == E_INVALID
+    assert call(keep=0) == E_INVALID
+    assert call(keep=9) == E_INVALID
+    assert call(out=7) == E_DTYPE
+    assert lib.sparsp_attn_workspace_bytes(ctypes.byref(g), 0) == E_INVALID
+    bad = geom(i0=3, i1=3)
+    assert lib.sparsp_attn_workspace_bytes(ctypes.byref(bad), 1) == E_INVALID
+    gf = geom(H=2, L=1000, d=64, block=64, i0=0, i1=4, dtype=sp.F32)
+    assert lib.sparsp_attn_workspace_bytes(ctypes.byref(gf), 4) == 0   # float32: no split
