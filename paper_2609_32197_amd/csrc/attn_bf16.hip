@@ -873,58 +873,71 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     if (lse && g == 0 && store) lse[orow] = lse_out;
 }
 
+constexpr int kMaxTailSplit = 4;  // pieces per split tail row, at most
+
 // Merge of the pieces of the split tail rows. Piece p of tail row t sits in
 // workspace slot t * tail_k + p as (O_p normalised by its own sum, lse_p in
 // natural log); the pieces cover disjoint parts of the row's kept blocks, so
 // with m = max_p lse_p and w_p = exp(lse_p - m)
 //   O = sum_p w_p O_p / sum_p w_p,   lse = m + log sum_p w_p
-// (the online-softmax merge of Section 2.3). One workgroup per tail row;
-// rows whose pieces are all empty (padded queries) get O = 0, lse = -inf.
+// (the online-softmax merge of Section 2.3). Rows whose pieces are all
+// empty (padded queries) get O = 0, lse = -inf. One thread per float4 of
+// output: a workgroup covers 256 / (D/4) query rows of one tail row, and each
+// thread issues the loads of all the row's pieces at once.
 template <int D, int BLK, bool OUT_BF16>
 __global__ __launch_bounds__(256) void tail_merge_kernel(
     const float* __restrict__ part_o, const float* __restrict__ part_lse, void* __restrict__ O,
     float* __restrict__ lse, int G, int nq, int h_lo, int tail_first, int tail_k) {
-    const int t = blockIdx.x;
+    constexpr int C4 = D / 4;             // float4 per query row
+    constexpr int QPW = 256 / C4;         // query rows per workgroup
+    constexpr int WPR = BLK / QPW;        // workgroups per tail row
+    const int t = blockIdx.x / WPR;
+    const int q = (blockIdx.x % WPR) * QPW + threadIdx.x / C4, c4 = threadIdx.x % C4;
     const int row = xcd_row(tail_first + t, G);
     const int h = h_lo + row / nq, r = row % nq;
-    const int64_t orow0 = (int64_t(h) * nq + r) * BLK;
-    constexpr int C4 = D / 4;
-    for (int e = threadIdx.x; e < BLK * C4; e += blockDim.x) {
-        const int q = e / C4, c4 = e % C4;
-        float m = -INFINITY;
-        for (int p = 0; p < tail_k; ++p)
-            m = fmaxf(m, part_lse[(int64_t(t) * tail_k + p) * BLK + q]);
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        float wsum = 0.f;
-        if (m != -INFINITY)
-            for (int p = 0; p < tail_k; ++p) {
-                const int64_t prow = (int64_t(t) * tail_k + p) * BLK + q;
-                const float lp = part_lse[prow];
-                if (lp == -INFINITY) continue;
-                const float w = expf(lp - m);
-                const float4 x = reinterpret_cast<const float4*>(part_o + prow * D)[c4];
-                wsum += w;
-                acc.x += w * x.x;
-                acc.y += w * x.y;
-                acc.z += w * x.z;
-                acc.w += w * x.w;
-            }
-        const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
-        const int64_t at = (orow0 + q) * D + 4 * c4;
-        if constexpr (OUT_BF16) {
-            uint2 wv;
-            wv.x = f32_to_bf16_bits(acc.x * inv) | (f32_to_bf16_bits(acc.y * inv) << 16);
-            wv.y = f32_to_bf16_bits(acc.z * inv) | (f32_to_bf16_bits(acc.w * inv) << 16);
-            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(O) + at) = wv;
+    const int64_t orow = (int64_t(h) * nq + r) * BLK + q;
+    float lp[kMaxTailSplit];
+    float4 x[kMaxTailSplit];
+    float m = -INFINITY;
+#pragma unroll
+    for (int p = 0; p < kMaxTailSplit; ++p) {
+        if (p < tail_k) {
+            const int64_t prow = (int64_t(t) * tail_k + p) * BLK + q;
+            lp[p] = part_lse[prow];
+            x[p] = reinterpret_cast<const float4*>(part_o + prow * D)[c4];
+            m = fmaxf(m, lp[p]);
         } else {
-            *reinterpret_cast<float4*>(static_cast<float*>(O) + at) =
-                make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+            lp[p] = -INFINITY;
         }
-        if (c4 == 0 && lse) lse[orow0 + q] = wsum > 0.f ? m + logf(wsum) : -INFINITY;
     }
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float wsum = 0.f;
+    if (m != -INFINITY) {
+#pragma unroll
+        for (int p = 0; p < kMaxTailSplit; ++p) {
+            if (lp[p] == -INFINITY) continue;
+            const float w = expf(lp[p] - m);
+            wsum += w;
+            acc.x += w * x[p].x;
+            acc.y += w * x[p].y;
+            acc.z += w * x[p].z;
+            acc.w += w * x[p].w;
+        }
+    }
+    const float inv = wsum > 0.f ? 1.0f / wsum : 0.f;
+    const int64_t at = orow * D + 4 * c4;
+    if constexpr (OUT_BF16) {
+        uint2 wv;
+        wv.x = f32_to_bf16_bits(acc.x * inv) | (f32_to_bf16_bits(acc.y * inv) << 16);
+        wv.y = f32_to_bf16_bits(acc.z * inv) | (f32_to_bf16_bits(acc.w * inv) << 16);
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(O) + at) = wv;
+    } else {
+        *reinterpret_cast<float4*>(static_cast<float*>(O) + at) =
+            make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+    }
+    if (c4 == 0 && lse) lse[orow] = wsum > 0.f ? m + logf(wsum) : -INFINITY;
 }
 
-constexpr int kMaxTailSplit = 4;
 
 // Workgroups of `kernel` that are resident at once on the current device.
 template <typename Kernel>
@@ -959,8 +972,9 @@ hipError_t launch_tail_merge(const Geom& g, const AttnPart& part, const TailPlan
                              const float* part_o, const float* part_lse, void* O, float* lse,
                              hipStream_t s) {
     const int S = G - tp.first;
-    tail_merge_kernel<D, BLK, OUT><<<S, 256, 0, s>>>(part_o, part_lse, O, lse, G, g.nq, part.h_lo,
-                                                     tp.first, tp.k);
+    constexpr int wpr = BLK / (256 / (D / 4));  // workgroups per tail row
+    tail_merge_kernel<D, BLK, OUT><<<S * wpr, 256, 0, s>>>(part_o, part_lse, O, lse, G, g.nq,
+                                                           part.h_lo, tp.first, tp.k);
     return hipGetLastError();
 }
 
