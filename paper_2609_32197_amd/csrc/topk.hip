@@ -227,10 +227,10 @@ hipError_t launch_cdf_s(const Geom& g, const float* scores, float tau, const Glo
 //   4. the queues interleaved: entry k of queue x goes to the position that a
 //      round-robin walk over the queues gives it, i.e. x + 8k while all
 //      queues are that long.
-// A count outside [0, n] is clamped into it. The head totals are summed over
-// all rows at once (LDS atomics), and each queue's pass walks only the rows
-// of its own heads; up to kCountCache rows, the counts are read from memory
-// once and kept in LDS.
+// A count outside [0, n] is clamped into it. Up to kCountCache rows the
+// counts are read from memory once and kept in LDS, where one thread per head
+// sums its total; past that, all rows add into the totals with LDS atomics.
+// Each queue's pass walks only the rows of its own heads.
 constexpr int kXcds = 8;
 constexpr int kCountCache = 14336;  // rows whose counts are kept in LDS (16 bits each)
 static_assert(kMaxBlocks < 65536, "counts must fit 16 bits");
