@@ -54,6 +54,12 @@
 // rescaled) when some lane's block max exceeds it by more than 2^8, so most
 // blocks skip the rescale; probabilities then stay below 2^8, well inside
 // float32 and bf16 range, and the final normalisation uses the same max.
+//
+// Last round balanced (with a caller workspace). One workgroup per row leaves
+// the last round of resident workgroups partly empty; its rows can instead
+// run as up to four workgroups each, over consecutive parts of the row's
+// kept list, which write float32 partials that tail_merge_kernel folds
+// through their log-sum-exp. Every other row is computed as without it.
 #include "sparsp_internal.h"
 
 namespace sparsp {
