@@ -54,7 +54,10 @@ Readings taken where the paper is silent:
 * CDF mode per query block: the softmax of the row's float32 block scores over
   all n blocks; blocks ordered by (score descending, index ascending); the
   shortest prefix of that order whose mass reaches tau is kept, then the
-  diagonal and global blocks are added; tau in (0, 1];
+  diagonal and global blocks are added; tau in (0, 1]. "Reaches tau" is
+  decided on the mass the prefix leaves out (at most (1 - tau) of the total),
+  summed from the smallest block upward, and tau = 1 keeps every block, since
+  every block's softmax mass is positive; the scores must be finite;
 * a chunk is (owner shard, run of consecutive heads); shards are taken in
   ring order from the local one (r, r+1, ..., r+R-1 mod R); remote shards are
   cut into chunks of a given number of heads, the last remote shard into
@@ -109,6 +112,7 @@ __all__ = [
     "rank_demand",
     "remote_blocks",
     "cdf_order_and_mass",
+    "cdf_cut",
     "select_cdf",
     "provide_masks",
     "pack_by_consumer",
@@ -611,23 +615,42 @@ def remote_blocks(demand: np.ndarray, owner: np.ndarray, rank: int) -> int:
 # ---------------------------------------------------------------------------
 
 def cdf_order_and_mass(score_row: np.ndarray) -> tuple:
-    """The CDF order of one row and the cumulative softmax mass along it.
+    """The CDF order of one row and the softmax mass each prefix leaves out.
 
-    score_row: float32 [n]. Returns (order int64 [n]: blocks by score
-    descending, then index ascending; mass float64 [n]: mass[k] is the softmax
-    mass of the first k+1 blocks of that order, mass[n-1] = 1).
+    score_row: float32 [n]. Returns (order, left, Z): order int64 [n] lists the
+    blocks by score descending, then index ascending; p_j = exp(S_j - max S)
+    (unnormalised softmax weights) and Z = sum_j p_j; left float64 [n + 1] is
+    the mass left out by the first k blocks of the order, left[k] = sum of
+    p over order[k:], summed from the smallest weight upward (so a prefix's
+    left-out mass is resolved down to the smallest weight, not to the rounding
+    of a running total near Z); left[0] = Z and left[n] = 0.
     """
     s = np.asarray(score_row)
     if s.dtype != np.float32:
         raise TypeError("scores must be float32")
-    if np.isnan(s).any():
-        raise ValueError("NaN block score")
+    if not np.isfinite(s).all():
+        raise ValueError("non-finite block score")
     s64 = s.astype(np.float64)
     order = np.lexsort((np.arange(s.shape[0]), -s64))
-    p = np.exp(s64 - s64.max())
-    mass = np.cumsum(p[order]) / p.sum()
-    mass[-1] = 1.0
-    return order.astype(np.int64), mass
+    p = np.exp(s64 - s64.max())[order]
+    left = np.zeros(s.shape[0] + 1, dtype=np.float64)
+    left[:-1] = np.cumsum(p[::-1])[::-1]
+    return order.astype(np.int64), left, float(left[0])
+
+
+def cdf_cut(left: np.ndarray, Z: float, tau: float) -> int:
+    """Length of the shortest prefix of the CDF order whose mass reaches tau Z.
+
+    A prefix's mass reaches tau Z exactly when the mass it leaves out is at
+    most (1 - tau) Z. Every block carries strictly positive mass, so tau = 1
+    keeps all n blocks (float64 exp can underflow to 0 for very low scores;
+    the definition, not the rounding, decides that case).
+    """
+    n = left.shape[0] - 1
+    if tau >= 1.0:
+        return n
+    budget = (1.0 - tau) * Z
+    return int(np.argmax(left[1:] <= budget)) + 1  # left[n] = 0, so some k qualifies
 
 
 def select_cdf(scores: np.ndarray, tau: float, i0: int, global_blocks: Sequence[int] = ()) -> tuple:
@@ -647,8 +670,8 @@ def select_cdf(scores: np.ndarray, tau: float, i0: int, global_blocks: Sequence[
     mask = np.zeros((H, nq, n), dtype=bool)
     for h in range(H):
         for r in range(nq):
-            order, mass = cdf_order_and_mass(s[h, r])
-            k = int(np.argmax(mass >= tau)) + 1
+            order, left, Z = cdf_order_and_mass(s[h, r])
+            k = cdf_cut(left, Z, tau)
             mask[h, r, order[:k]] = True
             for j in forced_blocks(i0 + r, G):
                 mask[h, r, j] = True
