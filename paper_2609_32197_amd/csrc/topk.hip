@@ -7,13 +7,14 @@
 // bits of mask word s: a ballot builds a mask word directly.
 //
 // Selection is exact and order-free. Scores become order-preserving 32-bit
-// keys (-0.0 folded onto +0.0, NaN below every number). A 32-step bitwise
-// search finds T, the k-th largest candidate key (k = keep - |F|): at each bit
-// it keeps the bit set if at least k candidates still reach the threshold.
+// keys (-0.0 folded onto +0.0). A 32-step bitwise search finds T, the k-th
+// largest candidate key (k = keep - |F|): at each bit it keeps the bit set if
+// at least k candidates still reach the threshold.
 // Candidates above T are taken; among those equal to T the lowest indices are
 // taken until k is reached, ranked in index order with ballots and
 // mbcnt. No floating point is involved, so the result is a pure function of
-// the score bits.
+// the score bits. NaN scores are outside the contract: a row holding one still
+// gets a well-formed selection of keep blocks, but which ones is unspecified.
 #include "sparsp_internal.h"
 
 namespace sparsp {
@@ -21,8 +22,7 @@ namespace {
 
 __device__ __forceinline__ uint32_t order_key(float x) {
     uint32_t u = __float_as_uint(x);
-    if (u == 0x80000000u) u = 0u;                                   // -0.0 ties +0.0
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0u;  // NaN: lowest
+    if (u == 0x80000000u) u = 0u;  // -0.0 ties +0.0
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
@@ -121,12 +121,16 @@ __device__ __forceinline__ float wave_max(float x) {
 // CDF-mode selection (Section 8.1), one wave per (head, local row), blocks held
 // as in topk_kernel. p_j = exp(s_j - max) over the row, Z = sum p. With the
 // blocks ordered by (score desc, index asc), the kept prefix is the shortest
-// one whose mass reaches tau Z: a bitwise search finds the largest order key T
-// whose upper set {key >= T} still holds mass >= tau Z; the blocks above T
-// are kept, and the blocks equal to T (equal scores, equal p) are added in
-// index order until the target is met. The diagonal and global blocks are
-// kept in any case. sel rows list the kept blocks ascending, then -1 up to n.
-// A NaN score counts as no mass and ranks below every number.
+// one whose mass reaches tau Z, i.e. whose left-out mass is at most
+// (1 - tau) Z. The left-out mass is summed from the blocks themselves, not
+// taken as Z minus a running total, so trailing blocks far below the total
+// still count. A bitwise search finds the largest order key T whose lower set
+// {key < T} carries at most that budget; the blocks at or above T are kept,
+// except that of the blocks equal to T (equal scores, equal p) the highest
+// indices are left out while the budget allows. tau = 1 keeps every block
+// (every block's mass is positive, even where float32 exp underflows). The
+// diagonal and global blocks are kept in any case. sel rows list the kept
+// blocks ascending, then -1 up to n. Scores must be finite.
 template <int S>
 __global__ __launch_bounds__(256) void cdf_kernel(const float* __restrict__ scores, int H, int nq,
                                                   int n, int W, int i0, float tau, GlobalSet gs,
@@ -150,41 +154,46 @@ __global__ __launch_bounds__(256) void cdf_kernel(const float* __restrict__ scor
         forced[s] = valid[s] && (j == i || ((gs.w[s] >> lane) & 1));
         const float v = valid[s] ? srow[j] : -INFINITY;
         key[s] = valid[s] ? order_key(v) : 0u;
-        x[s] = (v != v) ? -INFINITY : v;
+        x[s] = v;
         mx = fmaxf(mx, x[s]);
     }
     mx = wave_max(mx);
     float part = 0.f;
 #pragma unroll
     for (int s = 0; s < S; ++s) {
-        p[s] = (x[s] == -INFINITY) ? 0.f : expf(x[s] - mx);
+        p[s] = valid[s] ? expf(x[s] - mx) : 0.f;
         part += p[s];
     }
-    const float target = tau * wave_sum(part);
+    const bool keep_all = tau >= 1.0f;
+    const float budget = (1.0f - tau) * wave_sum(part);
 
     uint32_t T = 0;
-    for (int b = 31; b >= 0; --b) {
-        const uint32_t t = T | (1u << b);
-        float m = 0.f;
-#pragma unroll
-        for (int s = 0; s < S; ++s) m += (valid[s] && key[s] >= t) ? p[s] : 0.f;
-        if (wave_sum(m) >= target) T = t;
-    }
-    float above = 0.f, pt = 0.f;
-    int ties = 0;
-#pragma unroll
-    for (int s = 0; s < S; ++s) {
-        above += (valid[s] && key[s] > T) ? p[s] : 0.f;
-        const bool eq = valid[s] && key[s] == T;
-        pt = fmaxf(pt, eq ? p[s] : 0.f);
-        ties += popc64(__ballot(eq));
-    }
-    float acc = wave_sum(above);
-    pt = wave_max(pt);
     int need = 0;
-    while (need < ties && acc < target) {  // uniform: every lane holds the same values
-        acc += pt;
-        ++need;
+    if (!keep_all) {
+        for (int b = 31; b >= 0; --b) {
+            const uint32_t t = T | (1u << b);
+            float m = 0.f;
+#pragma unroll
+            for (int s = 0; s < S; ++s) m += (valid[s] && key[s] < t) ? p[s] : 0.f;
+            if (wave_sum(m) <= budget) T = t;
+        }
+        float below = 0.f, pt = 0.f;
+        int ties = 0;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            below += (valid[s] && key[s] < T) ? p[s] : 0.f;
+            const bool eq = valid[s] && key[s] == T;
+            pt = fmaxf(pt, eq ? p[s] : 0.f);
+            ties += popc64(__ballot(eq));
+        }
+        float left = wave_sum(below);
+        pt = wave_max(pt);
+        int out = 0;  // ties left out, the highest indices; at least one tie stays
+        while (out + 1 < ties && left + pt <= budget) {  // uniform across the wave
+            left += pt;
+            ++out;
+        }
+        need = ties - out;
     }
 
     uint64_t* mrow = mask + int64_t(row) * W;
@@ -196,7 +205,7 @@ __global__ __launch_bounds__(256) void cdf_kernel(const float* __restrict__ scor
         const uint64_t eqb = __ballot(eq);
         const bool take_eq = eq && (ties_seen + below_lane(eqb)) < need;
         ties_seen += popc64(eqb);
-        const bool take = forced[s] || (valid[s] && key[s] > T) || take_eq;
+        const bool take = forced[s] || (valid[s] && (keep_all || key[s] > T)) || take_eq;
         const uint64_t word = __ballot(take);
         if (s < W && lane == 0) mrow[s] = word;
         if (take) selrow[written + below_lane(word)] = lane + 64 * s;
