@@ -121,17 +121,19 @@ def read_traffic():
 
 def measured_peaks(sp, torch, copy_bytes: int, stream):
     """Practical ceilings on this part, beside the data-sheet peaks: the bf16
-    MFMA rate with register operands (the library's probe kernel, best of
-    three ~20 ms launches) and a plain device-to-device copy of copy_bytes
+    MFMA rate with register operands (the benchmark's probe kernel in
+    paper_2609_32197_amd.probe, outside libsparsp; best of three ~20 ms
+    launches) and a plain device-to-device copy of copy_bytes
     (read + write, mean of five)."""
     wgs, iters = 1024, 60000
     sink = torch.empty(wgs * 256, dtype=torch.float32, device="cuda")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    sp.sparsp_mfma_probe(1000, wgs, sink, stream=stream)
+    from paper_2609_32197_amd import probe
+    probe.run(1000, wgs, sink, stream=stream)
     best = 0.0
     for _ in range(3):
         e0.record(stream)
-        sp.sparsp_mfma_probe(iters, wgs, sink, stream=stream)
+        probe.run(iters, wgs, sink, stream=stream)
         e1.record(stream)
         torch.cuda.synchronize()
         best = max(best, wgs * iters * 524288 / (e0.elapsed_time(e1) * 1e-3) / 1e12)
@@ -188,9 +190,14 @@ def cpu_baseline(wl, q, k, v, budget_s):
     """Time the float64 oracle over whole heads of the same workload until the budget is spent."""
     import numpy as np
     import oracle as orc
+    blas = "unknown"
     try:
         from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+        pools = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        threads = max([p.get("num_threads", 1) for p in pools] or [1])
+        if pools:
+            blas = ", ".join(f"{p.get('internal_api')} {p.get('version')} "
+                             f"({p.get('num_threads')} threads)" for p in pools)
     except Exception:  # threadpoolctl missing: numpy's default pool
         threads = os.cpu_count() or 1
     flops = 0
@@ -216,6 +223,9 @@ def cpu_baseline(wl, q, k, v, budget_s):
         "value": flops / spent / 1e12,
         "unit": "TFLOP/s",
         "cores": int(threads),
+        "host_cpu_count": os.cpu_count(),
+        "host_cpus_usable": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None,
+        "blas": blas,
         "kind": "oracle",
         "sample": f"{heads} of {wl.H} heads, whole pipeline (pool, score, select, union, pack, "
                   f"attend) per head, {spent:.1f} s",
@@ -577,6 +587,7 @@ def main(argv=None) -> int:
             "global_blocks": len(wl.global_blocks), "seed": a.seed,
         },
         "stages_ms": stage_ms,
+        "stages_statistic": "mean over the timed steps of HIP events recorded on the calls' stream",
         "wall_ms_per_step": wall_ms,
         "cache_flushed_between_steps": flush is not None,
         "attention": {

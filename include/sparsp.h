@@ -87,8 +87,11 @@ int sparsp_block_scores(const sparsp_geom* g, const void* Q, const void* K, floa
  * For local row i (global block i0+i) of head h, the forced set is
  * F = {i0+i} U global_blocks. The row keeps F and the first keep - |F| other
  * blocks ordered by score descending, then block index ascending. Scores are
- * compared as float32 values (+0.0 equals -0.0); a NaN score ranks below every
- * number. `keep` counts every kept block, forced ones included.
+ * compared as float32 values (+0.0 equals -0.0; infinities order as usual).
+ * `keep` counts every kept block, forced ones included. A NaN score is outside
+ * the contract: the device cannot report it without a host round trip, so the
+ * call still writes a well-formed row of `keep` blocks, but which blocks is
+ * unspecified.
  *
  * scores: float32 [H, nq, n] device. global_blocks: HOST array of n_global
  * block indices (may be NULL when n_global == 0; duplicates are ignored;
@@ -109,8 +112,12 @@ int sparsp_topk_mask(const sparsp_geom* g, const float* scores, int32_t keep,
  * For local row i of head h: p_j = exp(S[h,i,j] - max_j S) / sum_j exp(...)
  * over all n blocks (float32); with the blocks ordered by score descending,
  * then index ascending, the row keeps the shortest prefix whose mass reaches
- * tau, plus F = {i0+i} U global_blocks. A NaN score has no mass and ranks
- * last. Scores compare as in sparsp_topk_mask.
+ * tau, plus F = {i0+i} U global_blocks. "Reaches tau" is decided on the mass
+ * the prefix leaves out: at most (1 - tau) of the total, summed from the
+ * left-out blocks themselves, so blocks far below the total still count;
+ * tau = 1 keeps every block. Scores compare as in sparsp_topk_mask and must
+ * be finite (an infinite or NaN score is outside the contract: the row is
+ * well-formed, its cut unspecified).
  *
  * tau in (0, 1]. Outputs: mask uint64 [H, nq, W]; sel int32 [H, nq, n], each
  * row the kept blocks ascending then -1 (attention skips -1, so pass n as
@@ -161,6 +168,10 @@ int sparsp_demand_union_gather(const sparsp_geom* g, const uint64_t* mask, const
  * lse: float32 [H, nq*block] or NULL. A sel entry outside [0, n), or whose
  * slot is -1 or >= capacity_blocks, is skipped (it contributes nothing).
  * bf16 inputs use bf16 matrix-core products with float32 accumulation.
+ * Q, K_packed and V_packed must hold finite values: the bf16 kernels are
+ * compiled without NaN semantics, so an infinite or NaN input gives
+ * unspecified outputs for the rows it reaches (memory accesses stay in
+ * bounds whatever the values).
  */
 int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t* sel,
                              int32_t keep, const int32_t* slot_of, const void* K_packed,
@@ -403,17 +414,6 @@ int sparsp_pack_for_consumers(const sparsp_geom* g, const uint64_t* demands, int
  */
 int sparsp_route_volume(const sparsp_geom* g, const uint64_t* demands, int32_t ranks,
                         int32_t producer, int64_t* dense, int64_t* relay, int64_t* direct);
-
-/*
- * Measurement helper, not a step of the method: runs `workgroups` workgroups
- * of 256 threads, each wave issuing 4 * iters bf16 32x32x16 matrix-core
- * operations on register operands (no memory traffic), i.e.
- * workgroups * 4 * 4 * iters * 32768 FLOP, and writes one float per thread to
- * sink (device, workgroups * 256 floats, caller-owned; the values are
- * meaningless). Timing it gives the sustained bf16 MFMA rate of the part.
- * Errors: iters < 1, workgroups < 1 or > 1 << 20, NULL sink.
- */
-int sparsp_mfma_probe(int64_t iters, int32_t workgroups, float* sink, void* stream);
 
 /* Message of the calling thread's most recent error ("" if none). */
 const char* sparsp_last_error(void);

@@ -182,7 +182,6 @@ _SIGNATURES = {
     "sparsp_route_volume": [ctypes.POINTER(_Geom), _VP, _I32, _I32,
                             ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64),
                             ctypes.POINTER(ctypes.c_int64)],
-    "sparsp_mfma_probe": [ctypes.c_int64, _I32, _VP, _VP],
     "sparsp_row_order": [ctypes.POINTER(_Geom), _VP, _VP, _VP],
     "sparsp_block_sparse_attn_ordered": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP, _VP,
                                          _VP, ctypes.c_int64, ctypes.c_float, _VP, _VP,
@@ -660,16 +659,6 @@ def sparsp_route_volume(geom: Geometry, demands, ranks: int, producer: int) -> d
                                               int(producer), ctypes.byref(dense),
                                               ctypes.byref(relay), ctypes.byref(direct)))
     return {"dense": dense.value, "relay": relay.value, "direct": direct.value}
-
-
-def sparsp_mfma_probe(iters: int, workgroups: int, sink, stream=None) -> None:
-    """Enqueue the register-only bf16 MFMA rate probe (workgroups * 4 * 4 * iters
-    32x32x16 operations = workgroups * iters * 524,288 FLOP); sink: float32 cuda
-    tensor of at least workgroups * 256 elements."""
-    if sink.numel() < int(workgroups) * 256 or sink.dtype != _torch().float32 or not sink.is_cuda:
-        raise ValueError("sink must be a float32 cuda tensor of workgroups * 256 elements")
-    _check(load_library().sparsp_mfma_probe(int(iters), int(workgroups), sink.data_ptr(),
-                                            _stream(stream, sink.device)))
 
 
 block_scores = sparsp_block_scores

@@ -2,10 +2,15 @@
 
 Usage: python -m paper_2609_32197_amd.build [--jobs N] [--verbose]
 
-Each .hip file under csrc/ is compiled with hipcc for gfx950 only, then
-linked into paper_2609_32197_amd/libsparsp.so next to this file. Packed
-fp32 VALU instructions are disabled for device code (they are not used by
-these kernels and some of their forms are avoided on purpose).
+Each .hip file under csrc/ is compiled with hipcc for gfx950 only; each .cpp
+file there (the C ABI layer and the pure host planning code, which use only
+the HIP runtime API) with the host C++ compiler. Both are linked into
+paper_2609_32197_amd/libsparsp.so next to this file. Packed fp32 VALU
+instructions are disabled for device code (they are not used by these kernels
+and some of their forms are avoided on purpose).
+
+The benchmark's measurement helper, probe/mfma_probe.hip, is built into its
+own library, probe/libmfma_probe.so: it is not part of libsparsp.
 """
 
 from __future__ import annotations
@@ -22,7 +27,23 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libsparsp.so")
+PROBE_SRC = os.path.join(HERE, "probe", "mfma_probe.hip")
+PROBE_LIB = os.path.join(HERE, "probe", "libmfma_probe.so")
 ARCH = "gfx950"
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+
+# Host-only C++ (no device code): the HIP runtime API headers, AMD platform.
+HOST_COMMON = [
+    "-O2",
+    "-std=c++17",
+    "-fPIC",
+    "-Wall",
+    "-Wextra",
+    "-Wno-unused-parameter",
+    "-D__HIP_PLATFORM_AMD__",
+    f"-I{os.path.join(ROCM, 'include')}",
+    f"-I{os.path.join(ROOT, 'include')}",
+]
 
 COMMON = [
     f"--offload-arch={ARCH}",
@@ -49,8 +70,19 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (set HIPCC or install ROCm)")
 
 
+def host_cxx() -> str:
+    for cand in (os.environ.get("CXX"), shutil.which("g++"), shutil.which("c++")):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("no host C++ compiler found (set CXX)")
+
+
 def sources() -> list:
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+
+
+def host_sources() -> list:
+    return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".cpp"))
 
 
 def _run(cmd, verbose):
@@ -76,10 +108,16 @@ def build(jobs: int = 8, verbose: bool = False) -> str:
     objs = [os.path.join(BUILD, os.path.basename(s)[:-4] + ".o") for s in srcs]
     cmds = [[cc, *COMMON, *PER_FILE.get(os.path.basename(s), []), "-c", s, "-o", o]
             for s, o in zip(srcs, objs)]
+    hsrcs = host_sources()
+    hobjs = [os.path.join(BUILD, os.path.basename(s)[:-4] + ".host.o") for s in hsrcs]
+    cmds += [[host_cxx(), *HOST_COMMON, "-c", s, "-o", o] for s, o in zip(hsrcs, hobjs)]
+    probe_tmp = PROBE_LIB + ".tmp"
+    cmds.append([cc, *COMMON, "-shared", PROBE_SRC, "-o", probe_tmp])
     with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
         list(ex.map(lambda c: _run(c, verbose), cmds))
+    os.replace(probe_tmp, PROBE_LIB)
     tmp = LIB + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, *hobjs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -1,12 +1,16 @@
 // C ABI of libsparsp: argument checking, geometry derivation and dispatch.
 //
 // Every check runs on the host before any launch, so a call that returns an
-// error has enqueued nothing. The library holds no device state.
+// error has enqueued nothing. The library holds no device state. This file is
+// plain host C++ on the HIP runtime API (it calls only the launchers of
+// sparsp_launch.h, hipGetLastError and hipGetErrorString), so it also builds
+// with a host compiler under the address and undefined-behaviour sanitizers.
 #include <cstdarg>
+#include <cstdint>
 #include <cstdio>
 #include <cstring>
 
-#include "sparsp_internal.h"
+#include "sparsp_launch.h"
 
 namespace {
 
@@ -170,14 +174,6 @@ int attn_whole(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t 
 extern "C" {
 
 int sparsp_version(void) { return 200; }  // 0.2.0
-
-int sparsp_mfma_probe(int64_t iters, int32_t workgroups, float* sink, void* stream) {
-    if (iters < 1 || workgroups < 1 || workgroups > (1 << 20) || !sink)
-        return fail(SPARSP_E_INVALID, "mfma_probe: iters=%lld workgroups=%d sink=%p",
-                    (long long)iters, workgroups, (void*)sink);
-    return hip_status(sparsp::launch_mfma_probe(iters, workgroups, sink, (hipStream_t)stream),
-                      "mfma_probe");
-}
 
 const char* sparsp_last_error(void) { return g_err; }
 

@@ -1,6 +1,5 @@
-// Host side of shard-by-shard attention (Section 2.3, Section 7).
-//
-// plan_chunks orders the work of rank r over the owners' KV shards:
+// Host side of shard-by-shard attention (Section 2.3, Section 7): running a
+// plan. The plan itself (plan_chunks, in host_plan.cpp) orders the work of rank r over the owners' KV shards:
 //   * shard p holds the blocks [floor(p n / R), floor((p+1) n / R));
 //   * the local shard (p = r) comes first and stays whole: one chunk with all
 //     heads (Section 7.1: it needs no transfer);
@@ -19,47 +18,9 @@
 // other chunk folds itself into them through the log-sum-exp inside the
 // attention kernel (query blocks with no kept block in the shard exit without
 // touching memory). Heads that no chunk covers end as the empty result.
-#include <algorithm>
-#include <vector>
-
 #include "sparsp_internal.h"
 
 namespace sparsp {
-
-int plan_chunks(const Geom& g, const uint64_t* demand, int ranks, int rank, int heads_per_chunk,
-                int tail_heads_per_chunk, sparsp_chunk* out, int max_chunks) {
-    auto count = [&](int h0, int h1, int lo, int hi) {
-        int c = 0;
-        for (int h = h0; h < h1; ++h)
-            for (int j = lo; j < hi; ++j) c += int((demand[int64_t(h) * g.W + (j >> 6)] >> (j & 63)) & 1);
-        return c;
-    };
-    auto shard = [&](int p, int* lo, int* hi) {
-        *lo = int(int64_t(p) * g.n / ranks);
-        *hi = int(int64_t(p + 1) * g.n / ranks);
-    };
-    std::vector<sparsp_chunk> plan;
-    int lo, hi;
-    shard(rank, &lo, &hi);
-    plan.push_back({rank, lo, hi, 0, g.H, count(0, g.H, lo, hi)});
-    for (int k = 1; k < ranks; ++k) {
-        const int p = (rank + k) % ranks;
-        shard(p, &lo, &hi);
-        const int size = k == ranks - 1 ? tail_heads_per_chunk : heads_per_chunk;
-        std::vector<sparsp_chunk> part;
-        for (int h0 = 0; h0 < g.H; h0 += size) {
-            const int h1 = std::min(g.H, h0 + size);
-            part.push_back({p, lo, hi, h0, h1, count(h0, h1, lo, hi)});
-        }
-        std::stable_sort(part.begin(), part.end(), [](const sparsp_chunk& a, const sparsp_chunk& b) {
-            return a.blocks != b.blocks ? a.blocks > b.blocks : a.head_begin < b.head_begin;
-        });
-        plan.insert(plan.end(), part.begin(), part.end());
-    }
-    if (int(plan.size()) > max_chunks) return -int(plan.size());
-    std::copy(plan.begin(), plan.end(), out);
-    return int(plan.size());
-}
 
 hipError_t run_chunks(const Geom& g, const void* Q, const int32_t* sel, int keep,
                       const int32_t* slot_of, const void* Kp, const void* Vp, int64_t capacity,

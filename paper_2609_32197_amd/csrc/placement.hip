@@ -1,4 +1,5 @@
-// Dependency-aware placement (Section 4.3, Eq. 4) and the Eq. 3 block count.
+// Dependency-aware placement (Section 4.3, Eq. 4): the block permutation on
+// the device. The host parts live in host_plan.cpp:
 //
 // periodic_placement (host): rank floor(G s / B) of Eq. 4 for every block, with
 // s / B read as the in-frame offset of the block's first token over the frame
@@ -25,9 +26,6 @@
 // remote_demand (host): sum over heads of the demanded blocks outside the
 // rank's own range [i0, i1) of the geometry, i.e. sum_{p != r} |D_{r,h,p}|
 // of Eq. 3 in the layout (placed or contiguous) the geometry describes.
-#include <algorithm>
-#include <vector>
-
 #include "sparsp_internal.h"
 
 namespace sparsp {
@@ -64,22 +62,6 @@ __global__ __launch_bounds__(256) void permute_kernel(const int32_t* __restrict_
 
 }  // namespace
 
-void periodic_placement(int L, int block, int frame_tokens, int ranks, int32_t* perm,
-                        int32_t* rank_begin) {
-    const int n = (L + block - 1) / block;
-    std::vector<int> owner(n);
-    for (int j = 0; j < n; ++j)
-        owner[j] = int(int64_t(ranks) * ((int64_t(j) * block) % frame_tokens) / frame_tokens);
-    if (L % block) owner[n - 1] = ranks - 1;
-    int k = 0;
-    for (int p = 0; p < ranks; ++p) {
-        rank_begin[p] = k;
-        for (int j = 0; j < n; ++j)
-            if (owner[j] == p) perm[k++] = j;
-    }
-    rank_begin[ranks] = k;
-}
-
 hipError_t launch_permute(const Geom& g, const int32_t* perm, const void* X, void* Y, bool inverse,
                           hipStream_t s) {
     (void)hipGetLastError();
@@ -87,43 +69,6 @@ hipError_t launch_permute(const Geom& g, const int32_t* perm, const void* X, voi
     permute_kernel<<<dim3(g.n, g.H), 256, 0, s>>>(perm, (const char*)X, (char*)Y, g.n, g.L,
                                                   g.block, row_bytes, inverse ? 1 : 0);
     return hipGetLastError();
-}
-
-void remote_demand(const Geom& g, const uint64_t* demand, int64_t* remote, int64_t* demanded) {
-    int64_t rem = 0, all = 0;
-    for (int h = 0; h < g.H; ++h)
-        for (int j = 0; j < g.n; ++j) {
-            if (!((demand[int64_t(h) * g.W + (j >> 6)] >> (j & 63)) & 1)) continue;
-            ++all;
-            if (j < g.i0 || j >= g.i1) ++rem;
-        }
-    *remote = rem;
-    *demanded = all;
-}
-
-void route_volume(const Geom& g, const uint64_t* demands, int ranks, int producer, int64_t* dense,
-                  int64_t* relay, int64_t* direct) {
-    const int lo = int(int64_t(producer) * g.n / ranks), hi = int(int64_t(producer + 1) * g.n / ranks);
-    int64_t rel = 0, dir = 0;
-    std::vector<uint64_t> down(g.W);
-    for (int h = 0; h < g.H; ++h) {
-        std::fill(down.begin(), down.end(), 0);
-        for (int k = ranks - 1; k >= 1; --k) {  // farthest consumer first: down = union of distance >= k
-            const int c = (producer + k) % ranks;
-            const uint64_t* dm = demands + (int64_t(c) * g.H + h) * g.W;
-            for (int j = lo; j < hi; ++j) {
-                const uint64_t bit = uint64_t(1) << (j & 63);
-                if (dm[j >> 6] & bit) {
-                    ++dir;
-                    down[j >> 6] |= bit;
-                }
-            }
-            for (int j = lo; j < hi; ++j) rel += int64_t((down[j >> 6] >> (j & 63)) & 1);
-        }
-    }
-    *dense = int64_t(ranks - 1) * g.H * (hi - lo);
-    *relay = rel;
-    *direct = dir;
 }
 
 }  // namespace sparsp

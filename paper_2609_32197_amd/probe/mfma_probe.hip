@@ -1,4 +1,5 @@
-// Measurement helper, not a step of the method: the sustained rate of the
+// Measurement helper for the benchmark, not a step of the method and not
+// part of libsparsp or its C ABI: the sustained rate of the
 // bf16 matrix cores with every operand in registers (no memory traffic, no
 // softmax), the practical ceiling the attention kernel is compared with
 // beside the data-sheet peak. Each wave runs four independent accumulation
@@ -6,9 +7,9 @@
 // [-1, 1) (random bits switch more of the datapath than constants, and the
 // clock under the power limit depends on it). The sums are written out so
 // that no MFMA can be dropped.
-#include "sparsp_internal.h"
+#include <hip/hip_runtime.h>
+#include <stdint.h>
 
-namespace sparsp {
 namespace {
 
 typedef __bf16 bf16x8_p __attribute__((ext_vector_type(8)));
@@ -43,10 +44,15 @@ __global__ __launch_bounds__(256) void mfma_probe_kernel(int64_t iters, float* _
 
 }  // namespace
 
-hipError_t launch_mfma_probe(int64_t iters, int workgroups, float* sink, hipStream_t s) {
+// Runs `workgroups` workgroups of 256 threads, each wave issuing 4 * iters
+// bf16 32x32x16 matrix-core operations on register operands, i.e.
+// workgroups * iters * 524,288 FLOP, on `stream` (a hipStream_t), and writes
+// one float per thread to sink (device, workgroups * 256 floats; the values
+// are meaningless). Returns 0, -1 for iters < 1, workgroups outside
+// [1, 2^20] or a NULL sink (nothing launched), or -5 for a launch error.
+extern "C" int mfma_probe_run(int64_t iters, int32_t workgroups, float* sink, void* stream) {
+    if (iters < 1 || workgroups < 1 || workgroups > (1 << 20) || !sink) return -1;
     (void)hipGetLastError();
-    mfma_probe_kernel<<<workgroups, 256, 0, s>>>(iters, sink);
-    return hipGetLastError();
+    mfma_probe_kernel<<<workgroups, 256, 0, (hipStream_t)stream>>>(iters, sink);
+    return hipGetLastError() == hipSuccess ? 0 : -5;
 }
-
-}  // namespace sparsp

@@ -335,11 +335,14 @@ def test_routing_rejected(lib):
                                    ctypes.byref(z)) == E_INVALID
 
 
-def test_mfma_probe_rejected(lib):
-    assert lib.sparsp_mfma_probe(0, 4, P, None) == E_INVALID
-    assert lib.sparsp_mfma_probe(10, 0, P, None) == E_INVALID
-    assert lib.sparsp_mfma_probe(10, (1 << 20) + 1, P, None) == E_INVALID
-    assert lib.sparsp_mfma_probe(10, 4, None, None) == E_INVALID
+def test_mfma_probe_is_outside_the_abi(lib):
+    """The benchmark's MFMA probe lives in its own library, not in libsparsp."""
+    from paper_2609_32197_amd import probe
+    assert not hasattr(lib, "sparsp_mfma_probe")
+    assert probe.status(0, 4, P) == E_INVALID
+    assert probe.status(10, 0, P) == E_INVALID
+    assert probe.status(10, (1 << 20) + 1, P) == E_INVALID
+    assert probe.status(10, 4, None) == E_INVALID
 
 
 def test_row_order_and_ordered_attention_rejected(lib):

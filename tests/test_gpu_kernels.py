@@ -226,12 +226,13 @@ def test_errors_surface_through_the_binding(gpu):
 
 
 def test_mfma_probe_runs(gpu):
-    """The measurement probe: every thread writes a finite sum."""
+    """The benchmark's measurement probe: every thread writes a finite sum."""
+    from paper_2609_32197_amd import probe
     torch = P.torch()
     sink = torch.full((8 * 256,), float("nan"), dtype=torch.float32, device="cuda")
-    sp.sparsp_mfma_probe(50, 8, sink)
+    probe.run(50, 8, sink)
     torch.cuda.synchronize()
     out = sink.cpu()
     assert torch.isfinite(out).all() and (out != 0).any()
     with pytest.raises(ValueError):
-        sp.sparsp_mfma_probe(50, 9, sink)
+        probe.run(50, 9, sink)
