@@ -1,0 +1,151 @@
+"""Every (head, query block) row of attention against the oracle, at full size,
+in the launch the benchmark times: the Wan-style rank share (H=40, d=128,
+block 128, 147 local query blocks of 591, keep 89) and each density of the
+text-token sweep (H=48, d=64, block 64, 139 local query blocks of 278, keep
+14 / 28 / 70 / 139 / 278, four always-kept text blocks).
+
+The path runs exactly as bench.py's step: GPU block scores, GPU top-k mask,
+demand union and gather into buffers of capacity H*n, then the balanced
+attention call (sparsp_block_sparse_attn_balanced through the binding's
+workspace= argument, workspace sized by sparsp_attn_workspace_bytes), bf16
+output with lse. So the rows of the last round that the call splits into
+pieces and merges are among the rows checked.
+
+* The GPU mask must equal the oracle's selection from the GPU's own float32
+  scores, bit for bit (the mask is a pure function of the score bits).
+* The oracle (float64) then evaluates Eq. 1 over that mask for every row,
+  reading K and V directly, not through the packed buffers. Bar per row
+  (128 or 64 query tokens x d): max-abs <= 2e-2 and mean-abs <= 1e-3 on the
+  bf16 O, lse within 1e-4, padded query rows O = 0 and lse = -inf.
+* Determinism: the whole step run a second time into fresh buffers gives
+  bitwise the same mask, sel, demand, offsets, slot map, gather list, packed
+  K and V, O and lse.
+
+The heads are split over several tests so that each stays short; the GPU
+step runs once per workload. The oracle's rows are evaluated on a pool of
+host threads (numpy releases the interpreter lock in its products and
+exponentials), each with a single-threaded BLAS; the arithmetic of each row is
+the oracle's own.
+"""
+
+import functools
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+
+import oracle as orc
+import paper_2609_32197_amd as sp
+from tests import _parity as P
+
+pytestmark = pytest.mark.gpu
+
+WORKLOADS = ["wan-share", "text-sweep-5", "text-sweep-10", "text-sweep-25", "text-sweep-50",
+             "text-sweep-100"]
+GROUPS = 8
+_SAME = {}  # workload -> determinism result, kept after the large arrays are dropped
+
+
+def _step(wl, g, Q, K, V):
+    """bench.py's step: the four calls with its buffer shapes and workspace."""
+    torch = P.torch()
+    cap = wl.H * wl.n
+    _, _, sc = sp.sparsp_block_scores(g, Q, K)
+    m, sel = sp.sparsp_topk_mask(g, sc, wl.keep, wl.global_blocks)
+    packed = sp.sparsp_demand_union_gather(g, m, K, V, cap)
+    ws_bytes = sp.sparsp_attn_workspace_bytes(g, wl.keep)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda") if ws_bytes > 0 else None
+    O, lse = sp.sparsp_block_sparse_attn(g, Q, sel, packed["slot_of"], packed["K_packed"],
+                                         packed["V_packed"], wl.softmax_scale,
+                                         out_dtype=sp.BF16, workspace=ws)
+    torch.cuda.synchronize()
+    return sc, m, sel, packed, O, lse, ws_bytes
+
+
+@functools.lru_cache(maxsize=1)
+def _run(name):
+    torch = P.torch()
+    from workloads import get_workload, make_qkv
+    wl = get_workload(name)
+    q, k, v = make_qkv(wl)
+    g = P.geometry(wl.H, wl.L, wl.d, wl.block, wl.i0, wl.i1, wl.dtype)
+    Q, K, V = (P.to_device(x, wl.dtype) for x in (q, k, v))
+    sc, m, sel, packed, O, lse, ws_bytes = _step(wl, g, Q, K, V)
+    # determinism: the same step into fresh buffers
+    sc2, m2, sel2, packed2, O2, lse2, _ = _step(wl, g, Q, K, V)
+    same = {
+        "scores": torch.equal(sc.view(torch.int32), sc2.view(torch.int32)),
+        "mask": torch.equal(m, m2), "sel": torch.equal(sel, sel2),
+        "O": torch.equal(O.view(torch.int16), O2.view(torch.int16)),
+        "lse": torch.equal(lse.view(torch.int32), lse2.view(torch.int32)),
+    }
+    S = int(packed["head_off"][-1].item())
+    for key in ("demand", "head_off", "slot_of"):
+        same[key] = torch.equal(packed[key], packed2[key])
+    same["gather_blk"] = torch.equal(packed["gather_blk"][:S], packed2["gather_blk"][:S])
+    for key in ("K_packed", "V_packed"):
+        same[key] = torch.equal(packed[key][:S].view(torch.int16), packed2[key][:S].view(torch.int16))
+    del sc2, m2, sel2, packed2, O2, lse2
+    _SAME[name] = same
+    res = dict(wl=wl, q=q, k=k, v=v, scores=sc.cpu().numpy(), mask_words=m.cpu().numpy(),
+               O=O.float().cpu().numpy(), lse=lse.cpu().numpy(), same=same, ws_bytes=ws_bytes)
+    del Q, K, V, sc, m, sel, packed, O, lse
+    torch.cuda.empty_cache()
+    return res
+
+
+CASES = [(name, grp) for name in WORKLOADS for grp in range(GROUPS)]
+
+
+@pytest.mark.parametrize("name,grp", CASES, ids=[f"{n}-heads{g}of{GROUPS}" for n, g in CASES])
+def test_every_row_against_oracle(gpu, name, grp):
+    res = _run(name)
+    wl = res["wl"]
+    n, b = wl.n, wl.block
+    mask = orc.words_to_mask(res["mask_words"].view(np.uint64), n)
+    heads = [h for h in range(wl.H) if h % GROUPS == grp]
+    if grp == 0:
+        ref_mask, _ = orc.select_topk(res["scores"], wl.keep, wl.i0, wl.global_blocks)
+        np.testing.assert_array_equal(mask, ref_mask)
+    else:
+        ref_mask, _ = orc.select_topk(res["scores"][heads], wl.keep, wl.i0, wl.global_blocks)
+        np.testing.assert_array_equal(mask[heads], ref_mask)
+    worst = worst_lse = 0.0
+    abs_sum = count = 0.0
+    dec = {h: tuple(orc.decode_input(x[h], wl.dtype) for x in (res["q"], res["k"], res["v"]))
+           for h in heads}
+
+    def oracle_row(hr):
+        h, r = hr
+        qf, kf, vf = dec[h]
+        return orc.attend_block(qf, kf, vf, mask[h, r], wl.i0 + r, wl.L, b, wl.softmax_scale)
+
+    pairs = [(h, r) for h in heads for r in range(wl.nq)]
+    workers = min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 4)
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(1), ThreadPoolExecutor(workers) as ex:
+        refs = list(ex.map(oracle_row, pairs))
+    for (h, r), (o_ref, l_ref) in zip(pairs, refs):
+        got = res["O"][h, r * b:(r + 1) * b]
+        mx, mean = P.check_attention(got, o_ref, True, f"{name} h={h} r={r}")
+        worst = max(worst, mx)
+        abs_sum += mean * got.size
+        count += got.size
+        lg = res["lse"][h, r * b:(r + 1) * b]
+        fin = np.isfinite(l_ref)
+        assert (np.isneginf(lg) == ~fin).all(), f"{name} h={h} r={r}: padded rows"
+        assert (got[~fin] == 0).all()
+        lerr = float(np.abs(lg[fin] - l_ref[fin]).max())
+        assert lerr <= 1e-4, f"{name} h={h} r={r}: lse off by {lerr:.3g}"
+        worst_lse = max(worst_lse, lerr)
+    print(f"\n[attention error] {name} heads {heads[0]}..{heads[-1]} step {GROUPS}: "
+          f"{len(heads) * wl.nq} rows, max-abs {worst:.3g}, mean-abs {abs_sum / count:.3g}, "
+          f"lse max {worst_lse:.3g}, workspace {res['ws_bytes']} B")
+
+
+@pytest.mark.parametrize("name", WORKLOADS)
+def test_step_is_deterministic(gpu, name):
+    same = _SAME[name] if name in _SAME else _run(name)["same"]
+    bad = [k for k, ok in same.items() if not ok]
+    assert not bad, f"{name}: outputs differ between two runs of the step: {bad}"
