@@ -50,16 +50,18 @@
 // 8*(l/32) .. +7; B lane l holds column l%32, same k values; the 16 results
 // of lane l are column l%32, rows 8*(r/4) + 4*(l/32) + r%4.
 //
-// The running max is refreshed lazily: it only moves (and the accumulator is
-// rescaled) when some lane's block max exceeds it by more than 2^8, so most
-// blocks skip the rescale; probabilities then stay below 2^8, well inside
-// float32 and bf16 range, and the final normalisation uses the same max.
-//
-// Last round balanced (with a caller workspace). One workgroup per row leaves
-// the last round of resident workgroups partly empty; its rows can instead
-// run as up to four workgroups each, over consecutive parts of the row's
-// kept list, which write float32 partials that tail_merge_kernel folds
-// through their log-sum-exp. Every other row is computed as without it.
+// The running max m moves (and the accumulator is rescaled) when some lane's
+// block max exceeds it by more than a per-lane threshold t (log2 units). t is
+// 8 at most, which keeps every probability below 2^8, and smaller while the
+// mass the lane has accumulated is small: after each rescale, once the block
+// is accumulated, t = clamp(log2(l) - 2, 0, 8) for the lane's mass l. A block
+// whose top probability 2^(max - m) would carry more than a quarter of that
+// mass therefore enters with its max exactly at m, i.e. probability exactly
+// 1, which bf16 represents exactly. On peaked rows, where O is close to a few
+// V rows, the bf16 rounding of those few probabilities would otherwise be the
+// largest error of O. Between rescales l only grows, so t errs on the side of
+// moving the max; on spread rows t reaches several units after the first
+// block and most blocks skip the rescale.
 #include "sparsp_internal.h"
 
 namespace sparsp {
@@ -72,6 +74,13 @@ typedef float floatx8 __attribute__((ext_vector_type(8)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
+
+// The rescale threshold for a lane that has accumulated mass l (units of its
+// running max): moving the max pays off once a block's top probability would
+// exceed l / 4, and is forced beyond 2^8.
+__device__ __forceinline__ float rescale_threshold(float l) {
+    return fminf(kRescaleThreshold, fmaxf(0.f, __log2f(l) - 2.f));
+}
 
 __device__ __forceinline__ int sigma(int m) {  // swap bits 2 and 3
     return (m & ~0xC) | ((m & 4) << 1) | ((m & 8) >> 1);
@@ -334,8 +343,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     floatx16 oacc[C::DT];
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = floatx16{};
-    float m_run = -INFINITY;  // running (lazy) max of scaled scores, log2 units
+    float m_run = -INFINITY;  // running max of scaled scores, log2 units
     float l_run = 0.f;        // this lane's partial row sum
+    float t_run = 0.f;        // rescale threshold (see above)
     const int last_cnt = L - (L / BLK) * BLK;  // valid keys of a partial last block
 
     for (int jj = 0; jj < nkeep; ++jj) {
@@ -413,9 +423,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 #pragma unroll
             for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(fmaxf(mx, s[mt][rr]), s[mt][rr + 1]);
         mx = pair_max(mx) * c2;
-        // Lazy max: move it only when some lane's block max exceeds it by more
-        // than the threshold (always on the first block a lane sees).
-        if (__ballot(mx > m_run + kRescaleThreshold)) {
+        // The max moves by the rule above (always on the first block a lane sees).
+        const bool moved = __ballot(mx > m_run + t_run) != 0;
+        if (moved) {
             const float m_new = fmaxf(m_run, mx);
             const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
@@ -441,6 +451,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[t][dt], pb, oacc[dt], 0, 0, 0);
         }
         l_run += lsum[0] + lsum[1];
+        if (moved) t_run = rescale_threshold(l_run);
     }
 
     // Merge the two key halves of each query group through their log-sum-exp.
@@ -683,7 +694,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     floatx16 oacc[C::DT];
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = floatx16{};
-    float m_run = -INFINITY, l_run = 0.f;
+    float m_run = -INFINITY, l_run = 0.f, t_run = 0.f;  // t_run: rescale threshold
     const int last_cnt = L - (L / BLK) * BLK;
 
     // Entering block jj: K(jj) and V(jj) are in flight, K issued first.
@@ -749,7 +760,8 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 #pragma unroll
             for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(fmaxf(mx, s[mt][rr]), s[mt][rr + 1]);
         mx = pair_max(mx) * c2;
-        if (__ballot(mx > m_run + kRescaleThreshold)) {
+        const bool moved = __ballot(mx > m_run + t_run) != 0;
+        if (moved) {
             const float m_new = fmaxf(m_run, mx);
             const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
@@ -805,6 +817,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         }
         __builtin_amdgcn_s_setprio(0);
         l_run += lsum[0] + lsum[1];
+        if (moved) t_run = rescale_threshold(l_run);
 
         wait_vmem_all();   // K(jj+1) landed
         __syncthreads();   // K(jj+1) visible; every wave is done with V(jj)
