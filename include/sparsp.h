@@ -216,6 +216,30 @@ int sparsp_block_sparse_attn_balanced(const sparsp_geom* g, const void* Q, const
                                       float* lse, void* stream);
 
 /*
+ * sparsp_block_sparse_attn_balanced for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the float32 partials of the split last-round rows go to a
+ * fixed device array of the library instead of a caller workspace. The array
+ * holds 36 MiB per GPU the library runs on and stays allocated until the
+ * process ends; the call itself allocates and frees nothing.
+ *   - Outputs are those of sparsp_block_sparse_attn_balanced with a workspace
+ *     of sparsp_attn_workspace_bytes(g, keep) bytes, bit for bit.
+ *   - Every call on a GPU shares that GPU's array. Calls that overlap on one
+ *     GPU (different streams, or different host threads without ordering)
+ *     race for it and must not be issued; stream-ordered calls are fine.
+ * Errors: those of sparsp_block_sparse_attn; SPARSP_E_CAPACITY when the tail
+ * split would need more than the fixed array (sparsp_attn_workspace_bytes
+ * above 36 MiB; no supported shape does on a 256-CU part); SPARSP_E_HIP when
+ * the array's device address cannot be obtained.
+ */
+int sparsp_block_sparse_attn_balanced_noalloc(const sparsp_geom* g, const void* Q,
+                                              const int32_t* sel, int32_t keep,
+                                              const int32_t* slot_of, const void* K_packed,
+                                              const void* V_packed, int64_t capacity_blocks,
+                                              float softmax_scale, void* O, int32_t out_dtype,
+                                              float* lse, void* stream);
+
+/*
  * Longest-first row order, for selections whose rows keep different numbers of
  * blocks (CDF mode, Section 8.1): a row whose kept list is several times the
  * mean otherwise starts late and sets the attention time alone.

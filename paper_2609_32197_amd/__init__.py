@@ -190,6 +190,9 @@ _SIGNATURES = {
     "sparsp_block_sparse_attn_balanced": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32, _VP,
                                           _VP, _VP, ctypes.c_int64, ctypes.c_float, _VP,
                                           ctypes.c_int64, _VP, ctypes.c_int32, _VP, _VP],
+    "sparsp_block_sparse_attn_balanced_noalloc": [ctypes.POINTER(_Geom), _VP, _VP, ctypes.c_int32,
+                                                  _VP, _VP, _VP, ctypes.c_int64, ctypes.c_float,
+                                                  _VP, ctypes.c_int32, _VP, _VP],
 }
 _RESTYPES = {"sparsp_attn_workspace_bytes": ctypes.c_int64}
 
@@ -376,14 +379,17 @@ def sparsp_demand_union_gather(geom: Geometry, mask, K, V, capacity_blocks: Opti
 def sparsp_block_sparse_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed,
                              softmax_scale: Optional[float] = None, out_dtype: Optional[int] = None,
                              O=None, lse=None, want_lse: bool = True, stream=None, row_order=None,
-                             workspace=None):
+                             workspace=None, fixed_scratch: bool = False):
     """Block-sparse attention. Returns (O [H, nq*block, d], lse [H, nq*block] or None).
 
     With row_order (int32 [H*nq], e.g. from sparsp_row_order) the rows are
     launched in that order (sparsp_block_sparse_attn_ordered); the outputs are
     the same bit for bit. With workspace (a device tensor, e.g. of
     sparsp_attn_workspace_bytes(geom, keep) bytes) the rows of the last round
-    of workgroups are split to fill the GPU (sparsp_block_sparse_attn_balanced)."""
+    of workgroups are split to fill the GPU (sparsp_block_sparse_attn_balanced).
+    With fixed_scratch the same split uses the library's fixed device array
+    instead (sparsp_block_sparse_attn_balanced_noalloc; pass O and lse as well
+    for a call that allocates nothing)."""
     torch = _torch()
     g = geom
     et = _elem_dtype(g)
@@ -411,9 +417,12 @@ def sparsp_block_sparse_attn(geom: Geometry, Q, sel, slot_of, K_packed, V_packed
     )
     gs = g.c_struct()
     lib = load_library()
-    if row_order is not None and workspace is not None:
-        raise ValueError("row_order and workspace cannot be combined")
-    if workspace is not None:
+    if sum(x is not None and x is not False for x in (row_order, workspace, fixed_scratch)) > 1:
+        raise ValueError("row_order, workspace and fixed_scratch cannot be combined")
+    if fixed_scratch:
+        _check(lib.sparsp_block_sparse_attn_balanced_noalloc(ctypes.byref(gs), *args,
+                                                             _stream(stream, Q.device)))
+    elif workspace is not None:
         if not workspace.is_cuda or not workspace.is_contiguous():
             raise ValueError("workspace must be a contiguous cuda tensor")
         _check(lib.sparsp_block_sparse_attn_balanced(

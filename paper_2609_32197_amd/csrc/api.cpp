@@ -135,11 +135,16 @@ int check_part(const sparsp::Geom& G, int kv_lo, int kv_hi, int h_lo, int h_hi) 
     return SPARSP_OK;
 }
 
+// How the bf16 launch may split the rows of its last round: not at all, into
+// a caller workspace, or into the library's fixed scratch array.
+enum class TailSpace { kNone, kWorkspace, kScratch };
+
 int attn_whole(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t keep,
                const int32_t* slot_of, const void* K_packed, const void* V_packed,
                int64_t capacity_blocks, float softmax_scale, const int32_t* order, void* O,
                int32_t out_dtype, float* lse, void* stream, const char* what,
-               void* workspace = nullptr, int64_t workspace_bytes = 0) {
+               void* workspace = nullptr, int64_t workspace_bytes = 0,
+               TailSpace tail = TailSpace::kNone) {
     sparsp::Geom G;
     if (int rc = derive(g, &G)) return rc;
     if (!O) return fail(SPARSP_E_INVALID, "NULL tensor pointer");
@@ -153,12 +158,24 @@ int attn_whole(const sparsp_geom* g, const void* Q, const int32_t* sel, int32_t 
         return fail(SPARSP_E_DTYPE, "f32 inputs produce f32 output only");
     sparsp::AttnPart whole{0, G.n, 0, G.H, 0};
     whole.order = order;
-    if (workspace && workspace_bytes > 0) {
+    if (tail == TailSpace::kWorkspace && workspace && workspace_bytes > 0) {
         if (!aligned16(workspace)) return fail(SPARSP_E_INVALID, "workspace must be 16-byte aligned");
         whole.ws = workspace;
         whole.ws_bytes = workspace_bytes;
     }
     hipStream_t s = (hipStream_t)stream;
+    if (tail == TailSpace::kScratch && G.bf16) {
+        const int64_t need = sparsp::attn_tail_workspace_bytes(G, keep);
+        if (need > sparsp::kScratchBytes)
+            return fail(SPARSP_E_CAPACITY,
+                        "%s: the tail split needs %lld bytes, the fixed scratch holds %lld", what,
+                        (long long)need, (long long)sparsp::kScratchBytes);
+        return hip_status(sparsp::launch_attn_bf16_noalloc(G, Q, sel, keep, slot_of, K_packed,
+                                                           V_packed, capacity_blocks,
+                                                           softmax_scale, O,
+                                                           out_dtype == SPARSP_BF16, lse, s),
+                          what);
+    }
     hipError_t e =
         G.bf16 ? sparsp::launch_attn_bf16(G, Q, sel, keep, slot_of, K_packed, V_packed,
                                           capacity_blocks, softmax_scale, whole, O,
@@ -276,7 +293,20 @@ int sparsp_block_sparse_attn_balanced(const sparsp_geom* g, const void* Q, const
     if (workspace_bytes < 0) return fail(SPARSP_E_INVALID, "workspace_bytes < 0");
     return attn_whole(g, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
                       softmax_scale, nullptr, O, out_dtype, lse, stream,
-                      "sparsp_block_sparse_attn_balanced", workspace, workspace_bytes);
+                      "sparsp_block_sparse_attn_balanced", workspace, workspace_bytes,
+                      TailSpace::kWorkspace);
+}
+
+int sparsp_block_sparse_attn_balanced_noalloc(const sparsp_geom* g, const void* Q,
+                                              const int32_t* sel, int32_t keep,
+                                              const int32_t* slot_of, const void* K_packed,
+                                              const void* V_packed, int64_t capacity_blocks,
+                                              float softmax_scale, void* O, int32_t out_dtype,
+                                              float* lse, void* stream) {
+    return attn_whole(g, Q, sel, keep, slot_of, K_packed, V_packed, capacity_blocks,
+                      softmax_scale, nullptr, O, out_dtype, lse, stream,
+                      "sparsp_block_sparse_attn_balanced_noalloc", nullptr, 0,
+                      TailSpace::kScratch);
 }
 
 int sparsp_block_sparse_attn_ordered(const sparsp_geom* g, const void* Q, const int32_t* sel,

@@ -83,6 +83,19 @@ hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, in
 // when it does not apply): one float32 partial block per resident slot.
 int64_t attn_tail_workspace_bytes(const Geom& g, int keep);
 
+// Size of the fixed device array that the no-allocation attention entry point
+// uses in place of a workspace (per GPU; 36 MiB holds the largest tail split
+// of the supported shapes on a 256-CU part: 512 slots x 128 x 129 x 4 bytes).
+constexpr int64_t kScratchBytes = int64_t(36) << 20;
+
+// The bf16 attention of the whole geometry with the tail split's partials in
+// that fixed array (the caller has checked attn_tail_workspace_bytes against
+// kScratchBytes).
+hipError_t launch_attn_bf16_noalloc(const Geom& g, const void* Q, const int32_t* sel, int keep,
+                                    const int32_t* slot_of, const void* Kp, const void* Vp,
+                                    int64_t capacity, float scale, void* O, bool out_bf16,
+                                    float* lse, hipStream_t s);
+
 hipError_t launch_attn_f32(const Geom& g, const float* Q, const int32_t* sel, int keep,
                            const int32_t* slot_of, const float* Kp, const float* Vp,
                            int64_t capacity, float scale, const AttnPart& part, float* O,

@@ -171,6 +171,20 @@ int main() {
         REJECT(bal(P, 1 << 20, 4, 7), E_DTYPE);
         ACCEPT(bal(P, 1 << 20), 1);
         ACCEPT(bal(nullptr, 0), 1);
+        auto noalloc = [&](int keep, int out, const sparsp_geom* gg) {
+            return sparsp_block_sparse_attn_balanced_noalloc(gg, P, at<int32_t>(), keep,
+                                                             at<int32_t>(), P, P, 16, 0.1f, P, out,
+                                                             nullptr, nullptr);
+        };
+        REJECT(noalloc(0, SPARSP_BF16, &g), E_INVALID);
+        REJECT(noalloc(9, SPARSP_BF16, &g), E_INVALID);
+        REJECT(noalloc(4, 7, &g), E_DTYPE);
+        REJECT(noalloc(4, SPARSP_BF16, nullptr), E_INVALID);
+        ACCEPT(noalloc(4, SPARSP_BF16, &g), 1);
+        // the stand-in's workspace for 512 slots at d = 128 (33.8 MB) fits the fixed
+        // 36 MiB array; at d = 256 (f32 only) the call takes the f32 path, no scratch
+        auto g32 = geom(2, 1024, 64, 128, 0, 8, SPARSP_F32);
+        ACCEPT(noalloc(4, SPARSP_F32, &g32), 1);
         REJECT(sparsp_attn_workspace_bytes(&g, 0), E_INVALID);
         auto bad = geom(2, 1024, 128, 128, 3, 3);
         REJECT(sparsp_attn_workspace_bytes(&bad, 4), E_INVALID);

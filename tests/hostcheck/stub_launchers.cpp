@@ -42,6 +42,9 @@ hipError_t launch_attn_bf16(const Geom&, const void*, const int32_t*, int, const
 int64_t attn_tail_workspace_bytes(const Geom& g, int) {
     return int64_t(512) * g.block * (g.d + 1) * 4;  // 512 resident slots
 }
+hipError_t launch_attn_bf16_noalloc(const Geom&, const void*, const int32_t*, int, const int32_t*,
+                                    const void*, const void*, int64_t, float, void*, bool, float*,
+                                    hipStream_t) { return launched(); }
 hipError_t launch_attn_f32(const Geom&, const float*, const int32_t*, int, const int32_t*,
                            const float*, const float*, int64_t, float, const AttnPart&, float*,
                            float*, hipStream_t) { return launched(); }
