@@ -180,19 +180,28 @@ int sparsp_block_sparse_attn(const sparsp_geom* g, const void* Q, const int32_t*
 
 /*
  * Bytes of device workspace that sparsp_block_sparse_attn_balanced can use for
- * this geometry and keep on the current device: one float32 partial block
+ * this geometry and keep on the current device: the row order (4 bytes per
+ * local row, padded to a multiple of 256), then one float32 partial block
  * (block x (d + 1) x 4 bytes) per workgroup the attention kernel keeps
- * resident at once. 0 when no split applies (float32 inputs). Returns the size
+ * resident at once. 0 when neither applies (float32 inputs). Returns the size
  * (>= 0) or a negative sparsp_status for a bad geometry or keep. Host only.
  */
 int64_t sparsp_attn_workspace_bytes(const sparsp_geom* g, int32_t keep);
 
 /*
- * sparsp_block_sparse_attn with a workspace that lets the last round of
- * workgroups fill the GPU. The launch runs one workgroup per local row: R =
- * H*nq rows on the P workgroups the device holds at once, so the last round
- * has only S = R mod P rows and most of the GPU idles while they run. With a
- * workspace, each of those S rows is split into k = min(4, P / S) workgroups,
+ * sparsp_block_sparse_attn with a workspace that lets the workgroups share
+ * the L2 better and the last round of workgroups fill the GPU.
+ *   - Row order: the first 4 * H * nq bytes (padded to 256) receive, per head,
+ *     the local rows ordered by their first kept block (sel[h, r, 0]; ties by
+ *     row index), and the rows are launched in that order. The positions are
+ *     dealt to the XCDs in contiguous ranges as in sparsp_block_sparse_attn,
+ *     so the workgroups an XCD runs together walk overlapping, ascending tile
+ *     sequences in step. A row's arithmetic does not depend on its position.
+ * The launch runs one workgroup per local row: R = H*nq rows on the P
+ * workgroups the device holds at once, so the last round (the last positions
+ * of that order) has only S = R mod P rows and most of the GPU idles while they
+ * run. With the rest of the workspace, each of those S rows is split into
+ * k = min(4, P / S) workgroups,
  * each over a consecutive part of the row's kept blocks. The pieces write
  * float32 partials (O normalised by its own sum, and lse) to the workspace,
  * and a second kernel merges each row's pieces through the log-sum-exp: the
@@ -202,9 +211,10 @@ int64_t sparsp_attn_workspace_bytes(const sparsp_geom* g, int32_t keep);
  *     float32 rounding only.
  *   - workspace: caller-owned device memory, 16-byte aligned; contents on entry
  *     do not matter and on return are unspecified. Calls that share a workspace
- *     must not overlap. With workspace NULL or workspace_bytes too small for
- *     k = 2, with S = 0, or with float32 inputs, the call is exactly
- *     sparsp_block_sparse_attn.
+ *     must not overlap. A workspace too small for the row order leaves the
+ *     natural order; one too small for k = 2 after the row order, or S = 0,
+ *     leaves no split. With workspace NULL or float32 inputs the call is
+ *     exactly sparsp_block_sparse_attn.
  * Errors: those of sparsp_block_sparse_attn; SPARSP_E_INVALID for a
  * misaligned workspace or workspace_bytes < 0.
  */
@@ -227,10 +237,11 @@ int sparsp_block_sparse_attn_balanced(const sparsp_geom* g, const void* Q, const
  *   - Every call on a GPU shares that GPU's array. Calls that overlap on one
  *     GPU (different streams, or different host threads without ordering)
  *     race for it and must not be issued; stream-ordered calls are fine.
- * Errors: those of sparsp_block_sparse_attn; SPARSP_E_CAPACITY when the tail
- * split would need more than the fixed array (sparsp_attn_workspace_bytes
- * above 36 MiB; no supported shape does on a 256-CU part); SPARSP_E_HIP when
- * the array's device address cannot be obtained.
+ * Errors: those of sparsp_block_sparse_attn; SPARSP_E_CAPACITY when the row
+ * order and the tail split would need more than the fixed array
+ * (sparsp_attn_workspace_bytes above 36 MiB: on a 256-CU part, more than
+ * 983,040 local rows at d = 128 with 128-token blocks); SPARSP_E_HIP when the
+ * array's device address cannot be obtained.
  */
 int sparsp_block_sparse_attn_balanced_noalloc(const sparsp_geom* g, const void* Q,
                                               const int32_t* sel, int32_t keep,

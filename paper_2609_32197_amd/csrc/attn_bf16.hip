@@ -116,6 +116,44 @@ __device__ __forceinline__ int xcd_row(int w, int G) {
     return xcd * per + min(xcd, rem) + idx;
 }
 
+// With row_sort (the balanced launch), position k of head h's rows holds row
+// row_sort[h * nq + k] of that head: the rows in the order of their first kept
+// block, so that the workgroups an XCD runs together walk overlapping tile
+// sequences in step and share more of its L2. Without it, positions are rows.
+__device__ __forceinline__ int sorted_row(int p, int nq, const int32_t* row_sort) {
+    if (!row_sort) return p;
+    const int r = row_sort[p];
+    return (p / nq) * nq + ((r >= 0 && r < nq) ? r : p % nq);
+}
+
+// Per head (one workgroup of 1024 threads): the local rows ordered by their
+// first kept block (sel rows are ascending, so that is sel[h, r, 0]; a row
+// whose list starts with -1 sorts last), ties by row index. row_sort[h * nq +
+// k] is the row at position k. Each rank is a count of smaller keys, so the
+// order is deterministic.
+__global__ __launch_bounds__(1024) void row_sort_kernel(const int32_t* __restrict__ sel, int keep,
+                                                        int nq, int n,
+                                                        int32_t* __restrict__ row_sort) {
+    __shared__ uint32_t key[kMaxBlocks];  // nq <= n <= kMaxBlocks
+    const int h = blockIdx.x;
+    const int32_t* srow = sel + int64_t(h) * nq * keep;
+    for (int r = threadIdx.x; r < nq; r += 1024) {
+        int j = srow[int64_t(r) * keep];
+        if (j < 0 || j >= n) j = n;
+        key[r] = uint32_t(j) * uint32_t(kMaxBlocks) + uint32_t(r);  // unique per row
+    }
+    __syncthreads();
+    for (int r = threadIdx.x; r < nq; r += 1024) {
+        const uint32_t mine = key[r];
+        int rank = 0;
+        for (int q = 0; q < nq; ++q) rank += key[q] < mine;
+        row_sort[int64_t(h) * nq + rank] = r;
+    }
+}
+
+// Bytes of the row order at the start of a balanced launch's workspace.
+int64_t row_sort_bytes(int rows) { return (int64_t(rows) * 4 + 255) / 256 * 256; }
+
 // Tail split: the rows of the last, partial round of workgroups (indices
 // tail_first .. G-1) run as tail_k workgroups each, so that round fills the
 // GPU. Workgroup tail_first + t*tail_k + p is piece p of tail row t, which
@@ -240,7 +278,8 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                       int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
                       int h_lo, int n_heads, int acc, int remap,
                       const int32_t* __restrict__ order, int tail_first, int tail_k,
-                      float* __restrict__ part_o, float* __restrict__ part_lse) {
+                      float* __restrict__ part_o, float* __restrict__ part_lse,
+                      const int32_t* __restrict__ row_sort) {
     using C = Cfg<D, BLK>;
     // [buffer][K tile | V tile]; reused for the final merge.
     __shared__ __attribute__((aligned(16))) uint16_t lds[2][2][C::TILE];
@@ -260,7 +299,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         wg = order[blockIdx.x];
         if (wg < 0 || wg >= G) return;
     } else if (remap) {
-        wg = xcd_row(tp.index, G);
+        wg = sorted_row(xcd_row(tp.index, G), nq, row_sort);
     } else {
         wg = tp.index;
     }
@@ -594,7 +633,8 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                     int64_t capacity, float c2 /* scale * log2(e) */, int kv_lo, int kv_hi,
                     int h_lo, int n_heads, int acc, int remap,
                     const int32_t* __restrict__ order, int tail_first, int tail_k,
-                    float* __restrict__ part_o, float* __restrict__ part_lse) {
+                    float* __restrict__ part_o, float* __restrict__ part_lse,
+                    const int32_t* __restrict__ row_sort) {
     using C = CfgRows<D, BLK>;
     __shared__ __attribute__((aligned(16))) uint16_t lk[C::TILE];
     __shared__ __attribute__((aligned(16))) uint16_t lv[C::TILE];
@@ -611,7 +651,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         wg = order[blockIdx.x];
         if (wg < 0 || wg >= G) return;
     } else if (remap) {
-        wg = xcd_row(tp.index, G);
+        wg = sorted_row(xcd_row(tp.index, G), nq, row_sort);
     } else {
         wg = tp.index;
     }
@@ -906,13 +946,14 @@ constexpr int kMaxTailSplit = 4;  // pieces per split tail row, at most
 template <int D, int BLK, bool OUT_BF16>
 __global__ __launch_bounds__(256) void tail_merge_kernel(
     const float* __restrict__ part_o, const float* __restrict__ part_lse, void* __restrict__ O,
-    float* __restrict__ lse, int G, int nq, int h_lo, int tail_first, int tail_k) {
+    float* __restrict__ lse, int G, int nq, int h_lo, int tail_first, int tail_k,
+    const int32_t* __restrict__ row_sort) {
     constexpr int C4 = D / 4;             // float4 per query row
     constexpr int QPW = 256 / C4;         // query rows per workgroup
     constexpr int WPR = BLK / QPW;        // workgroups per tail row
     const int t = blockIdx.x / WPR;
     const int q = (blockIdx.x % WPR) * QPW + threadIdx.x / C4, c4 = threadIdx.x % C4;
-    const int row = xcd_row(tail_first + t, G);
+    const int row = sorted_row(xcd_row(tail_first + t, G), nq, row_sort);
     const int h = h_lo + row / nq, r = row % nq;
     const int64_t orow = (int64_t(h) * nq + r) * BLK + q;
     float lp[kMaxTailSplit];
@@ -975,6 +1016,7 @@ int resident_slots(Kernel kernel, int threads, size_t dyn) {
 // large as the round's free slots, kMaxTailSplit and the workspace allow.
 struct TailPlan {
     int first, k;
+    const int32_t* row_sort = nullptr;
 };
 TailPlan plan_tail(int G, int slots, int64_t piece_bytes, int64_t ws_bytes) {
     if (slots <= 0) return {G, 1};
@@ -993,7 +1035,7 @@ hipError_t launch_tail_merge(const Geom& g, const AttnPart& part, const TailPlan
     const int S = G - tp.first;
     constexpr int wpr = BLK / (256 / (D / 4));  // workgroups per tail row
     tail_merge_kernel<D, BLK, OUT><<<S * wpr, 256, 0, s>>>(part_o, part_lse, O, lse, G, g.nq,
-                                                           part.h_lo, tp.first, tp.k);
+                                                           part.h_lo, tp.first, tp.k, tp.row_sort);
     return hipGetLastError();
 }
 
@@ -1008,6 +1050,34 @@ TailSpace tail_space(void* ws, const TailPlan& tp, int G, int D, int BLK) {
     return {o, o + pieces * BLK * D};
 }
 
+// The balanced launch's workspace holds the row order first (when it fits),
+// then the float32 partials of the tail split. Writes the order (one small
+// kernel on stream s) and returns the tail plan and where the partials go.
+template <typename Kernel>
+hipError_t balanced_plan(Kernel kernel, int threads, size_t dyn, const Geom& g,
+                         const AttnPart& part, const int32_t* sel, int keep, int G,
+                         int64_t piece_bytes, hipStream_t s, TailPlan* tp, void** partials) {
+    *tp = TailPlan{G, 1};
+    *partials = nullptr;
+    if (!part.ws || part.order || part.acc) return hipSuccess;
+    char* ws = static_cast<char*>(part.ws);
+    int64_t bytes = part.ws_bytes;
+    const int32_t* order = nullptr;
+    const int64_t sb = row_sort_bytes(G);
+    if (bytes >= sb) {
+        row_sort_kernel<<<part.h_hi - part.h_lo, 1024, 0, s>>>(
+            sel + int64_t(part.h_lo) * g.nq * keep, keep, g.nq, g.n, reinterpret_cast<int32_t*>(ws));
+        if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+        order = reinterpret_cast<const int32_t*>(ws);
+        ws += sb;
+        bytes -= sb;
+    }
+    *tp = plan_tail(G, resident_slots(kernel, threads, dyn), piece_bytes, bytes);
+    tp->row_sort = order;
+    *partials = ws;
+    return hipSuccess;
+}
+
 template <int D, int BLK>
 hipError_t launch_rows(const Geom& g, const void* Q, const int32_t* sel, int keep,
                      const int32_t* slot_of, const void* Kp, const void* Vp, int64_t cap,
@@ -1018,22 +1088,24 @@ hipError_t launch_rows(const Geom& g, const void* Q, const int32_t* sel, int kee
     const float c2 = scale * kLog2e;
     const size_t dyn = size_t(keep) * sizeof(int32_t);
     constexpr int THREADS = CfgRows<D, BLK>::THREADS;
-    TailPlan tp{G, 1};
-    if (part.ws && !part.order && !part.acc)
-        tp = plan_tail(G, resident_slots(attn_rows_kernel<D, BLK, true>, THREADS, dyn),
-                       int64_t(BLK) * (D + 1) * 4, part.ws_bytes);
-    const TailSpace ts = tp.k > 1 ? tail_space(part.ws, tp, G, D, BLK) : TailSpace{nullptr, nullptr};
+    TailPlan tp;
+    void* partials = nullptr;
+    if (hipError_t e = balanced_plan(attn_rows_kernel<D, BLK, true>, THREADS, dyn, g, part, sel,
+                                     keep, G, int64_t(BLK) * (D + 1) * 4, s, &tp, &partials);
+        e != hipSuccess)
+        return e;
+    const TailSpace ts = tp.k > 1 ? tail_space(partials, tp, G, D, BLK) : TailSpace{nullptr, nullptr};
     const int grid = tp.first + (G - tp.first) * tp.k;
     if (out_bf16)
         attn_rows_kernel<D, BLK, true><<<grid, THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, 1, part.order, tp.first, tp.k, ts.part_o, ts.part_lse);
+            part.acc, 1, part.order, tp.first, tp.k, ts.part_o, ts.part_lse, tp.row_sort);
     else
         attn_rows_kernel<D, BLK, false><<<grid, THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, 1, part.order, tp.first, tp.k, ts.part_o, ts.part_lse);
+            part.acc, 1, part.order, tp.first, tp.k, ts.part_o, ts.part_lse, tp.row_sort);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || tp.k < 2) return e;
     return out_bf16 ? launch_tail_merge<D, BLK, true>(g, part, tp, G, ts.part_o, ts.part_lse, O, lse, s)
@@ -1051,22 +1123,26 @@ hipError_t launch_shape(const Geom& g, const void* Q, const int32_t* sel, int ke
     const float c2 = scale * kLog2e;
     const int remap = 1;
     const size_t dyn = size_t(keep) * sizeof(int32_t);
-    TailPlan tp{G, 1};
-    if (part.ws && !part.order && !part.acc)
-        tp = plan_tail(G, resident_slots(attn_bf16_kernel<D, BLK, true>, C::THREADS, dyn),
-                       int64_t(BLK) * (D + 1) * 4, part.ws_bytes);
-    const TailSpace ts = tp.k > 1 ? tail_space(part.ws, tp, G, D, BLK) : TailSpace{nullptr, nullptr};
+    TailPlan tp;
+    void* partials = nullptr;
+    if (hipError_t e = balanced_plan(attn_bf16_kernel<D, BLK, true>, C::THREADS, dyn, g, part,
+                                     sel, keep, G, int64_t(BLK) * (D + 1) * 4, s, &tp, &partials);
+        e != hipSuccess)
+        return e;
+    const TailSpace ts = tp.k > 1 ? tail_space(partials, tp, G, D, BLK) : TailSpace{nullptr, nullptr};
     const int grid = tp.first + (G - tp.first) * tp.k;
     if (out_bf16)
         attn_bf16_kernel<D, BLK, true><<<grid, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, remap, part.order, tp.first, tp.k, ts.part_o, ts.part_lse);
+            part.acc, remap, part.order, tp.first, tp.k, ts.part_o, ts.part_lse,
+            tp.row_sort);
     else
         attn_bf16_kernel<D, BLK, false><<<grid, C::THREADS, dyn, s>>>(
             (const uint16_t*)Q, sel, slot_of, (const uint16_t*)Kp, (const uint16_t*)Vp, O, lse,
             g.L, g.n, g.i0, g.nq, keep, cap, c2, part.kv_lo, part.kv_hi, part.h_lo, n_heads,
-            part.acc, remap, part.order, tp.first, tp.k, ts.part_o, ts.part_lse);
+            part.acc, remap, part.order, tp.first, tp.k, ts.part_o, ts.part_lse,
+            tp.row_sort);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || tp.k < 2) return e;
     return out_bf16 ? launch_tail_merge<D, BLK, true>(g, part, tp, G, ts.part_o, ts.part_lse, O, lse, s)
@@ -1107,8 +1183,8 @@ int64_t attn_tail_workspace_bytes(const Geom& g, int keep) {
     else if (g.d == 128 && g.block == 64)
         slots = resident_slots(attn_bf16_kernel<128, 64, true>, Cfg<128, 64>::THREADS, dyn);
     if (slots <= 0) return 0;
-    // the tail pieces never outnumber the resident slots
-    return int64_t(slots) * g.block * (g.d + 1) * 4;
+    // the row order, then the tail pieces, which never outnumber the resident slots
+    return row_sort_bytes(g.H * g.nq) + int64_t(slots) * g.block * (g.d + 1) * 4;
 }
 
 }  // namespace sparsp

@@ -84,8 +84,9 @@ hipError_t launch_attn_bf16(const Geom& g, const void* Q, const int32_t* sel, in
 int64_t attn_tail_workspace_bytes(const Geom& g, int keep);
 
 // Size of the fixed device array that the no-allocation attention entry point
-// uses in place of a workspace (per GPU; 36 MiB holds the largest tail split
-// of the supported shapes on a 256-CU part: 512 slots x 128 x 129 x 4 bytes).
+// uses in place of a workspace (per GPU). 36 MiB holds the largest tail split
+// of the supported shapes on a 256-CU part (512 slots x 128 x 129 x 4 bytes =
+// 33.8 MB) plus the row order of up to 983,040 local rows.
 constexpr int64_t kScratchBytes = int64_t(36) << 20;
 
 // The bf16 attention of the whole geometry with the tail split's partials in

@@ -11,9 +11,14 @@ pieces, merged through the log-sum-exp. So:
 * without a workspace, or with one too small for two pieces, the call is
   sparsp_block_sparse_attn bit for bit.
 
-P is read back from sparsp_attn_workspace_bytes (one block x (d+1) float32
-partial per resident workgroup), and the rows of the last round are recomputed
-from the kernels' documented XCD-contiguous row order.
+The workspace holds the row order first (4 bytes per row, padded to 256),
+then one block x (d+1) float32 partial per resident workgroup, so P is read
+back from sparsp_attn_workspace_bytes. The rows of the last round are
+recomputed from the documented launch order: positions are dealt to the XCDs
+in contiguous ranges, and within each head position k holds the row with the
+k-th smallest first kept block (ties by row index). Rows the test takes as
+whole must then equal the plain call bit for bit, which also checks that
+order.
 """
 
 import numpy as np
@@ -33,16 +38,30 @@ def xcd_row(w, G):
     return x * per + min(x, rem) + idx
 
 
-def tail_rows(g, keep):
+def row_sort_bytes(rows):
+    return (rows * 4 + 255) // 256 * 256
+
+
+def sorted_rows(sel, n):
+    """Launch position -> row: within each head, rows by first kept block, then index."""
+    sel = np.asarray(sel)
+    H, nq = sel.shape[:2]
+    first = sel[:, :, 0].astype(np.int64)
+    first = np.where((first < 0) | (first >= n), n, first)
+    return np.concatenate([h * nq + np.lexsort((np.arange(nq), first[h])) for h in range(H)])
+
+
+def tail_rows(g, keep, sel):
     """Rows (h * nq + r) of the last round that the balanced call splits, and k."""
     nbytes = sp.sparsp_attn_workspace_bytes(g, keep)
-    slots = nbytes // (g.block * (g.d + 1) * 4)
     G = g.H * g.nq
+    slots = (nbytes - row_sort_bytes(G)) // (g.block * (g.d + 1) * 4)
     S = G % slots if slots else 0
     if S == 0 or slots // S < 2:
         return set(), 1, nbytes
     k = min(4, slots // S)
-    return {xcd_row(G - S + t, G) for t in range(S)}, k, nbytes
+    row_at = sorted_rows(sel.cpu().numpy() if hasattr(sel, "cpu") else sel, g.n)
+    return {int(row_at[xcd_row(G - S + t, G)]) for t in range(S)}, k, nbytes
 
 
 GEOMS = [
@@ -65,7 +84,7 @@ def test_balanced_attention(gpu, geo, keep_frac):
     g = P.geometry(H, L, d, b, i0, i1, dt)
     keep = max(1, int(round(keep_frac * n)))
     om, osel, sel, out = _pipeline(q, k, v, g, dt, keep)
-    split, kk, nbytes = tail_rows(g, keep)
+    split, kk, nbytes = tail_rows(g, keep, sel)
     assert nbytes > 0
     ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
     Qd = P.to_device(q, dt)
@@ -133,7 +152,7 @@ def test_balanced_full_size(gpu, name):
     m, sel = sp.sparsp_topk_mask(g, sc, wl.keep, wl.global_blocks)
     out = sp.sparsp_demand_union_gather(g, m, Kd, Vd)
     args = (g, Qd, sel, out["slot_of"], out["K_packed"], out["V_packed"], wl.softmax_scale)
-    split, kk, nbytes = tail_rows(g, wl.keep)
+    split, kk, nbytes = tail_rows(g, wl.keep, sel)
     ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device="cuda")
     O0, l0 = sp.sparsp_block_sparse_attn(*args)
     O1, l1 = sp.sparsp_block_sparse_attn(*args, workspace=ws)
