@@ -53,15 +53,16 @@
 // The running max m moves (and the accumulator is rescaled) when some lane's
 // block max exceeds it by more than a per-lane threshold t (log2 units). t is
 // 8 at most, which keeps every probability below 2^8, and smaller while the
-// mass the lane has accumulated is small: after each rescale, once the block
-// is accumulated, t = clamp(log2(l) - 2, 0, 8) for the lane's mass l. A block
-// whose top probability 2^(max - m) would carry more than a quarter of that
-// mass therefore enters with its max exactly at m, i.e. probability exactly
-// 1, which bf16 represents exactly. On peaked rows, where O is close to a few
-// V rows, the bf16 rounding of those few probabilities would otherwise be the
-// largest error of O. Between rescales l only grows, so t errs on the side of
-// moving the max; on spread rows t reaches several units after the first
-// block and most blocks skip the rescale.
+// mass the lane has accumulated is small: at each rescale, t = clamp(log2(l) -
+// 2, 0, 8) for the lane's mass l (rescaled to the new max, before the block is
+// added). A block whose top probability 2^(max - m) would carry more than a
+// quarter of the accumulated mass therefore enters with its max exactly at m,
+// i.e. probability exactly 1, which bf16 represents exactly. On peaked rows,
+// where O is close to a few V rows, the bf16 rounding of those few
+// probabilities would otherwise be the largest error of O. Between rescales l
+// only grows, so t errs on the side of moving the max; on spread rows t
+// reaches several units after the first blocks, and most blocks skip the
+// rescale (and the logarithm, which only rescale blocks compute).
 #include "sparsp_internal.h"
 
 namespace sparsp {
@@ -469,6 +470,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;
+            t_run = rescale_threshold(l_run);
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
         }
@@ -490,7 +492,6 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[t][dt], pb, oacc[dt], 0, 0, 0);
         }
         l_run += lsum[0] + lsum[1];
-        if (moved) t_run = rescale_threshold(l_run);
     }
 
     // Merge the two key halves of each query group through their log-sum-exp.
@@ -806,6 +807,7 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;
+            t_run = rescale_threshold(l_run);
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
         }
@@ -857,7 +859,6 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         }
         __builtin_amdgcn_s_setprio(0);
         l_run += lsum[0] + lsum[1];
-        if (moved) t_run = rescale_threshold(l_run);
 
         wait_vmem_all();   // K(jj+1) landed
         __syncthreads();   // K(jj+1) visible; every wave is done with V(jj)
