@@ -63,6 +63,8 @@
 // only grows, so t errs on the side of moving the max; on spread rows t
 // reaches several units after the first blocks, and most blocks skip the
 // rescale (and the logarithm, which only rescale blocks compute).
+#include <type_traits>
+
 #include "sparsp_internal.h"
 
 namespace sparsp {
@@ -388,8 +390,12 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     float t_run = 0.f;        // rescale threshold (see above)
     const int last_cnt = L - (L / BLK) * BLK;  // valid keys of a partial last block
 
-    for (int jj = 0; jj < nkeep; ++jj) {
-        const int buf = jj & 1;
+    // One block of the loop. The buffer index is a compile-time constant (the
+    // loop below is unrolled by two), so the LDS operand addresses of both
+    // buffers are per-lane constants plus an immediate offset, with no address
+    // arithmetic inside the loop.
+    auto step = [&](int jj, auto buf_c) {
+        constexpr int buf = decltype(buf_c)::value;
         const int cur = code;
         // A workgroup barrier does not wait for outstanding vector-memory
         // loads, and the compiler does not add that wait for direct-to-LDS
@@ -402,7 +408,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             code = next_code;
             next_code = (jj + 2 < nkeep) ? kept[jj + 2] : -1;
         }
-        if (cur < 0) continue;
+        if (cur < 0) return;
 
         const uint16_t* lk = &lds[buf][0][0];
         const uint16_t* lv = &lds[buf][1][0];
@@ -492,6 +498,10 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
                 oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[t][dt], pb, oacc[dt], 0, 0, 0);
         }
         l_run += lsum[0] + lsum[1];
+    };
+    for (int jj = 0; jj < nkeep; jj += 2) {
+        step(jj, std::integral_constant<int, 0>{});
+        if (jj + 1 < nkeep) step(jj + 1, std::integral_constant<int, 1>{});
     }
 
     // Merge the two key halves of each query group through their log-sum-exp.
