@@ -354,6 +354,7 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         vvoff[u] = chunk_src_offset<BLK>(p);
     }
     auto issue = [&](int code, int buf) {
+        code = __builtin_amdgcn_readfirstlane(code);  // wave-uniform: scalar address arithmetic
         const int64_t off = int64_t(code < 0 ? 0 : (code >> 1)) * C::TILE;
         copy_tile<C::NW, C::DMA>(Kp + off, C::TILE * 2, &lds[buf][0][0], kvoff, wave);
         copy_tile<C::NW, C::DMA>(Vp + off, C::TILE * 2, &lds[buf][1][0], vvoff, wave);
@@ -718,10 +719,14 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
         kvoff[u] = chunk_src_offset<D>(p);
         vvoff[u] = chunk_src_offset<BLK>(p);
     }
+    // (codes are wave-uniform; taking them into scalar registers keeps the
+    // copies' address arithmetic on the scalar unit)
     auto copy_k = [&](int code) {
+        code = __builtin_amdgcn_readfirstlane(code);
         copy_tile<C::NW, C::DMA>(Kp + int64_t(code >> 1) * C::TILE, C::TILE * 2, lk, kvoff, wave);
     };
     auto copy_v = [&](int code) {
+        code = __builtin_amdgcn_readfirstlane(code);
         copy_tile<C::NW, C::DMA>(Vp + int64_t(code >> 1) * C::TILE, C::TILE * 2, lv, vvoff, wave);
     };
 
