@@ -388,7 +388,9 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = floatx16{};
     float m_run = -INFINITY;  // running max of scaled scores, log2 units
     float l_run = 0.f;        // this lane's partial row sum
-    float t_run = 0.f;        // rescale threshold (see above)
+    // Set only where the max moves: lim = m_run + the rescale threshold (see
+    // above), neg_m = -m_run, or 0 while the lane has seen no finite score.
+    float lim = -INFINITY, neg_m = 0.f;
     const int last_cnt = L - (L / BLK) * BLK;  // valid keys of a partial last block
 
     // One block of the loop. The buffer index is a compile-time constant (the
@@ -471,27 +473,32 @@ void attn_bf16_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(fmaxf(mx, s[mt][rr]), s[mt][rr + 1]);
         mx = pair_max(mx) * c2;
         // The max moves by the rule above (always on the first block a lane sees).
-        const bool moved = __ballot(mx > m_run + t_run) != 0;
+        const bool moved = __ballot(mx > lim) != 0;
         if (moved) {
             const float m_new = fmaxf(m_run, mx);
             const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;
-            t_run = rescale_threshold(l_run);
+            lim = m_run + rescale_threshold(l_run);
+            neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
         }
-        const float m_use = (m_run == -INFINITY) ? 0.0f : m_run;
 
-        float lsum[2] = {0.f, 0.f};
+        // (the two partial sums start from the first two probabilities, not
+        // from 0 + p, which the compiler cannot drop)
+        float lsum[2];
 #pragma unroll
         for (int t = 0; t < C::PTW; ++t) {
             const int mt = t >> 1, hf = t & 1;
             floatx8 p;
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
-                p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, -m_use));
-                lsum[v & 1] += p[v];
+                p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, neg_m));
+                if (t == 0 && v < 2)
+                    lsum[v] = p[v];
+                else
+                    lsum[v & 1] += p[v];
             }
             const bf16x8 pb = __builtin_convertvector(p, bf16x8);
 #pragma unroll
@@ -750,7 +757,10 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
     floatx16 oacc[C::DT];
 #pragma unroll
     for (int dt = 0; dt < C::DT; ++dt) oacc[dt] = floatx16{};
-    float m_run = -INFINITY, l_run = 0.f, t_run = 0.f;  // t_run: rescale threshold
+    float m_run = -INFINITY, l_run = 0.f;
+    // Set only where the max moves: lim = m_run + the rescale threshold,
+    // neg_m = -m_run, or 0 while the lane has seen no finite score.
+    float lim = -INFINITY, neg_m = 0.f;
     const int last_cnt = L - (L / BLK) * BLK;
 
     // Entering block jj: K(jj) and V(jj) are in flight, K issued first.
@@ -816,20 +826,22 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
 #pragma unroll
             for (int rr = 0; rr < 16; rr += 2) mx = fmaxf(fmaxf(mx, s[mt][rr]), s[mt][rr + 1]);
         mx = pair_max(mx) * c2;
-        const bool moved = __ballot(mx > m_run + t_run) != 0;
+        const bool moved = __ballot(mx > lim) != 0;
         if (moved) {
             const float m_new = fmaxf(m_run, mx);
             const float alpha = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;
-            t_run = rescale_threshold(l_run);
+            lim = m_run + rescale_threshold(l_run);
+            neg_m = (m_run == -INFINITY) ? 0.f : -m_run;
 #pragma unroll
             for (int dt = 0; dt < C::DT; ++dt) oacc[dt] *= alpha;
         }
-        const float m_use = (m_run == -INFINITY) ? 0.0f : m_run;
 
         // 16-key steps; the V^T operands of step t+1 are read one step ahead.
-        float lsum[2] = {0.f, 0.f};
+        // (the two partial sums start from the first two probabilities, not
+        // from 0 + p, which the compiler cannot drop)
+        float lsum[2];
         bf16x8 vb[2][C::DT];
         auto vread = [&](int t, bf16x8 (&dst)[C::DT]) {
 #pragma unroll
@@ -847,8 +859,11 @@ void attn_rows_kernel(const uint16_t* __restrict__ Q, const int32_t* __restrict_
             floatx8 p;
 #pragma unroll
             for (int v = 0; v < 8; ++v) {
-                p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, -m_use));
-                lsum[v & 1] += p[v];
+                p[v] = __builtin_amdgcn_exp2f(fmaf(s[mt][8 * hf + v], c2, neg_m));
+                if (t == 0 && v < 2)
+                    lsum[v] = p[v];
+                else
+                    lsum[v & 1] += p[v];
             }
             return __builtin_convertvector(p, bf16x8);
         };
