@@ -596,7 +596,8 @@ def main(argv=None) -> int:
             "algorithmic_tflop": flops / 1e12,
             "kernel_ms": stage_ms["block_sparse_attn"],
             "tflops": attn_tflops,
-            "frac_of_mfma_peak": attn_tflops / peak,
+            "frac_of_mfma_peak": attn_tflops / peak if wl.dtype == "bf16" else None,
+            "frac_of_fp32_peak": attn_tflops / peak if wl.dtype != "bf16" else None,
             "measured_mfma_peak_tflops": mfma_meas,
             "frac_of_measured_mfma_peak": attn_tflops / mfma_meas if wl.dtype == "bf16" else None,
         },
@@ -611,7 +612,8 @@ def main(argv=None) -> int:
             "frac_of_measured_copy": gbytes / (stage_ms["demand_union_gather"] * 1e-3) / 1e9 / copy_meas,
         },
         "roofline": {
-            "bound": "mfma",
+            # the float32 path runs vector FMAs, not the matrix cores
+            "bound": "mfma" if wl.dtype == "bf16" else "alu",
             "achieved": attn_tflops,
             "peak": peak,
             "unit": "TFLOP/s",

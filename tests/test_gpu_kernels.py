@@ -142,7 +142,19 @@ def _pipeline(q, k, v, g, dt, keep, G=()):
     return om, osel, sel, out
 
 
-@pytest.mark.parametrize("geo", GEOMS, ids=lambda g: "H{}L{}d{}b{}_{}-{}_{}".format(*g))
+# The float32 kernel runs P = 4, 2 or 1 lanes per query row for blocks of up
+# to 64, 128 and 256 tokens; these cover each P with ragged blocks and odd d.
+F32_ATTN_GEOMS = [
+    (2, 1000, 20, 48, 1, 12, "f32"),     # P = 4, d = 20, ragged last block
+    (2, 1200, 96, 96, 0, 13, "f32"),     # P = 2, ragged (48 tokens)
+    (2, 1500, 128, 128, 2, 12, "f32"),   # P = 2, d = 128
+    (2, 1700, 64, 200, 0, 9, "f32"),     # P = 1, ragged (100 tokens)
+    (1, 2000, 128, 256, 0, 8, "f32"),    # P = 1, the largest block
+]
+
+
+@pytest.mark.parametrize("geo", GEOMS + F32_ATTN_GEOMS,
+                         ids=lambda g: "H{}L{}d{}b{}_{}-{}_{}".format(*g))
 @pytest.mark.parametrize("keep_frac", [0.3, 1.0])
 def test_attention_parity(gpu, geo, keep_frac):
     H, L, d, b, i0, i1, dt = geo
