@@ -2,7 +2,8 @@
 
 * The largest block count the library takes (n = 4096, the last block
   ragged) with every block kept: each row attends over 524,251 keys and its
-  kept list fills 16 KB of LDS beside the tiles.
+  kept list fills 16 KB of LDS beside the tiles (32 KB for the float32
+  kernel, whose case uses 16-token blocks).
 * The largest head count (H = 1024; the head offsets are staged in LDS by the
   offsets and gather kernels).
 * A sequence shorter than one block (n = 1: the whole sequence is one partial
@@ -70,6 +71,13 @@ def test_largest_block_count_dense_rows(gpu):
     # blocks, every block kept
     L = 4095 * 128 + 91
     _check((1, L, 128, 128, 4093, 4096, "bf16"), keep=4096, seed=11)
+
+
+def test_largest_block_count_dense_rows_f32(gpu):
+    # the float32 kernel with n = 4096 blocks of 16 (the last one 7 tokens),
+    # every block kept: its kept list (slots and counts) fills 32 KB of LDS
+    L = 4095 * 16 + 7
+    _check((1, L, 128, 16, 4094, 4096, "f32"), keep=4096, seed=14)
 
 
 def test_largest_head_count(gpu):
