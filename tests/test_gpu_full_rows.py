@@ -1,8 +1,10 @@
 """Every (head, query block) row of attention against the oracle, at full size,
 in the launch the benchmark times: the Wan-style rank share (H=40, d=128,
-block 128, 147 local query blocks of 591, keep 89) and each density of the
-text-token sweep (H=48, d=64, block 64, 139 local query blocks of 278, keep
-14 / 28 / 70 / 139 / 278, four always-kept text blocks).
+block 128, 147 local query blocks of 591, keep 89), the Hunyuan-style rank
+share (H=24, d=128, block 128, 116 local query blocks of 929, keep 93), the
+whole Hunyuan-style layer on one GPU (all 929 query blocks, keep 93) and
+each density of the text-token sweep (H=48, d=64, block 64, 139 local query
+blocks of 278, keep 14 / 28 / 70 / 139 / 278, four always-kept text blocks).
 
 The path runs exactly as bench.py's step: GPU block scores, GPU top-k mask,
 demand union and gather into buffers of capacity H*n, then the balanced
@@ -41,7 +43,7 @@ from tests import _parity as P
 
 pytestmark = pytest.mark.gpu
 
-WORKLOADS = ["wan-share", "text-sweep-5", "text-sweep-10", "text-sweep-25", "text-sweep-50",
+WORKLOADS = ["wan-share", "hunyuan-share", "hunyuan-layer", "text-sweep-5", "text-sweep-10", "text-sweep-25", "text-sweep-50",
              "text-sweep-100"]
 GROUPS = 8
 _SAME = {}  # workload -> determinism result, kept after the large arrays are dropped
