@@ -557,6 +557,9 @@ def main(argv=None) -> int:
     stage_ms = {nm: float(np.mean([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(a.steps)]))
                 for i, nm in enumerate(stage_names)}
     ms_per_step = float(np.mean([evs[s][0].elapsed_time(evs[s][4]) for s in range(a.steps)]))
+    stage_ms_median = {
+        nm: float(np.median([evs[s][i].elapsed_time(evs[s][i + 1]) for s in range(a.steps)]))
+        for i, nm in enumerate(stage_names)}
 
     sel = bufs["sel"].cpu().numpy()
     slot_of = packed["slot_of"].cpu().numpy()
@@ -588,6 +591,7 @@ def main(argv=None) -> int:
         },
         "stages_ms": stage_ms,
         "stages_statistic": "mean over the timed steps of HIP events recorded on the calls' stream",
+        "stages_ms_median": stage_ms_median,
         "wall_ms_per_step": wall_ms,
         "cache_flushed_between_steps": flush is not None,
         "attention": {
