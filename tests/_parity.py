@@ -102,3 +102,34 @@ def check_attention(O_gpu: np.ndarray, O_ref: np.ndarray, bf16: bool, what: str)
     else:
         assert mx <= F32_MAX_ABS, f"{what}: max {mx:.3g}"
     return mx, mean
+
+
+def check_every_row(q, k, v, mask, O_gpu: np.ndarray, lse_gpu: np.ndarray, wl, i0: int,
+                    nq: int, bf16: bool, what: str, lse_tol: float):
+    """Every (head, local query block) row of a full-size attention result against
+    the oracle's Eq. 1 over the given mask (the GPU's own), O at the parity bar,
+    lse within lse_tol, padded query rows lse = -inf. Heads run on a pool of host
+    threads, each with a single-threaded BLAS. Returns the largest max-abs error."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+    from threadpoolctl import threadpool_limits
+    b = wl.block
+
+    def head(h):
+        qf, kf, vf = (orc.decode_input(x[h], wl.dtype) for x in (q, k, v))
+        worst = 0.0
+        for r in range(nq):
+            o_ref, l_ref = orc.attend_block(qf, kf, vf, mask[h, r], i0 + r, wl.L, b,
+                                            wl.softmax_scale)
+            mx, _ = check_attention(O_gpu[h, r * b:(r + 1) * b], o_ref, bf16, f"{what} h={h} r={r}")
+            fin = np.isfinite(l_ref)
+            lg = lse_gpu[h, r * b:(r + 1) * b]
+            assert (np.isneginf(lg) == ~fin).all(), f"{what} h={h} r={r}: padded rows"
+            err = float(np.abs(lg[fin] - l_ref[fin]).max()) if fin.any() else 0.0
+            assert err <= lse_tol, f"{what} h={h} r={r}: lse off by {err:.3g}"
+            worst = max(worst, mx)
+        return worst
+
+    workers = min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 4)
+    with threadpool_limits(1), ThreadPoolExecutor(workers) as ex:
+        return max(ex.map(head, range(wl.H)))

@@ -154,28 +154,6 @@ def test_cdf_full_size_wan_share_and_attention(gpu):
     assert torch.equal(O.view(torch.int16), O2.view(torch.int16))
     assert torch.equal(lse.view(torch.int32), lse2.view(torch.int32))
     mask = orc.words_to_mask(m.cpu().numpy().view(np.uint64), g.n)
-    On, ln = O.float().cpu().numpy(), lse.cpu().numpy()
-    b = wl.block
-
-    def check_head(h):
-        qf, kf, vf = (orc.decode_input(x[h], wl.dtype) for x in (q, k, v))
-        worst = 0.0
-        for r in range(g.nq):
-            o_ref, l_ref = orc.attend_block(qf, kf, vf, mask[h, r], g.i0 + r, wl.L, b,
-                                            wl.softmax_scale)
-            mx, _ = P.check_attention(On[h, r * b:(r + 1) * b], o_ref, True,
-                                      f"cdf attention h={h} r={r}")
-            fin = np.isfinite(l_ref)
-            lg = ln[h, r * b:(r + 1) * b]
-            assert (np.isneginf(lg) == ~fin).all()
-            assert np.abs(lg[fin] - l_ref[fin]).max() <= 1e-4, (h, r)
-            worst = max(worst, mx)
-        return worst
-
-    import os
-    from concurrent.futures import ThreadPoolExecutor
-    from threadpoolctl import threadpool_limits
-    workers = min(16, len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else 4)
-    with threadpool_limits(1), ThreadPoolExecutor(workers) as ex:
-        worst = max(ex.map(check_head, range(wl.H)))
+    worst = P.check_every_row(q, k, v, mask, O.float().cpu().numpy(), lse.cpu().numpy(), wl,
+                              g.i0, g.nq, True, "cdf attention", 1e-4)
     print(f"\n[cdf attention] tau 0.9, {wl.H * g.nq} rows, max-abs {worst:.3g}")
