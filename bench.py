@@ -59,6 +59,9 @@ def parse_args(argv=None):
                          "Infinity Cache and L2 so each step starts cold)")
     ap.add_argument("--extensions", action="store_true",
                     help="also measure shard-by-shard attention, CDF selection, routing and placement")
+    ap.add_argument("--unit-probes", action="store_true",
+                    help="also measure the exponential, FMA and 16-byte LDS read issue rates "
+                         "against the register-only MFMA rate")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of this many MiB (for counter calibration)")
     return ap.parse_args(argv)
@@ -151,6 +154,45 @@ def measured_peaks(sp, torch, copy_bytes: int, stream):
     copy_gbps = 2 * n * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
     del src, dst
     return best, copy_gbps
+
+
+def measure_unit_probes(torch, stream, mfma_tflops: float, cus: int):
+    """Issue rates the attention kernel's softmax and operand reads depend on,
+    each best of three launches of its probe kernel (paper_2609_32197_amd.probe),
+    expressed per SIMD (per CU for LDS) and per matrix-core slot: the time one
+    v_mfma_f32_32x32x16_bf16 takes on a SIMD at the register-only MFMA rate of
+    the same process (32 cycles at that clock). The probes draw less power than
+    the MFMA probe, so their clock can run higher: the per-slot figures are
+    upper bounds for work that shares the SIMD with MFMAs."""
+    from paper_2609_32197_amd import probe
+    simds = 4 * cus
+    mfma_per_simd_s = mfma_tflops * 1e12 / 32768 / simds
+    out = {"mfma_tflops": mfma_tflops, "mfma_per_simd_per_s": mfma_per_simd_s}
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for kind, wgs, iters in (("exp", 8 * cus, 4000), ("fma", 8 * cus, 20000), ("lds", 2 * cus, 4000)):
+        sink = torch.empty(wgs * 256, dtype=torch.float32, device="cuda")
+        probe.run_unit(kind, 10, wgs, sink, stream=stream)
+        best = float("inf")
+        for _ in range(3):
+            e0.record(stream)
+            probe.run_unit(kind, iters, wgs, sink, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1) * 1e-3)
+        if kind == "lds":
+            per_cu_s = wgs * 4 * iters * 32 * 1024 / best / cus  # bytes per CU per second
+            out["lds"] = {"bytes_per_cu_per_s": per_cu_s,
+                          "bytes_per_cu_per_mfma_slot": per_cu_s / mfma_per_simd_s,
+                          "bytes_per_cycle_per_cu": per_cu_s / mfma_per_simd_s / 32,
+                          "workgroups": wgs, "seconds": best}
+        else:
+            per_simd_s = wgs * 4 * iters * 16 / best / simds  # wave instructions per SIMD per second
+            out[kind] = {"wave_instr_per_simd_per_s": per_simd_s,
+                         "per_mfma_slot": per_simd_s / mfma_per_simd_s,
+                         "cycles_per_wave_instr": 32 * mfma_per_simd_s / per_simd_s,
+                         "workgroups": wgs, "seconds": best}
+        del sink
+    return out
 
 
 def attention_flops(sel, L, block, i0, d):
@@ -570,6 +612,10 @@ def main(argv=None) -> int:
     demanded = int((slot_of >= 0).sum())
     traffic, traffic_note = read_traffic() if wl.name == "wan-share" else (None, "other workload")
     mfma_meas, copy_meas = measured_peaks(sp, torch, gbytes, stream)
+    unit = None
+    if a.unit_probes:
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        unit = measure_unit_probes(torch, stream, mfma_meas, cus)
 
     rec = {
         "metric": METRIC,
@@ -627,6 +673,8 @@ def main(argv=None) -> int:
         },
         "cpu_baseline": None,
     }
+    if unit is not None:
+        rec["unit_probes"] = unit
     if a.extensions and wl.ranks > 1:
         rec["chunked_attention"] = measure_chunked(sp, g, wl, Q, bufs, packed, stream, a)
         c = rec["chunked_attention"]

@@ -1,6 +1,7 @@
-"""The benchmark's measurement helper: a register-only bf16 MFMA loop that
+"""The benchmark's measurement helpers: a register-only bf16 MFMA loop that
 gives the sustained matrix-core rate of the part, the practical ceiling the
-attention kernel is compared with beside the data-sheet peak.
+attention kernel is compared with beside the data-sheet peak, and unit probes
+of the exponential, FMA and 16-byte LDS read issue rates.
 
 It is not a step of the method: it lives in its own library,
 libmfma_probe.so (built from mfma_probe.hip next to this file by the
@@ -26,6 +27,9 @@ def _load():
         _lib.mfma_probe_run.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
                                         ctypes.c_void_p]
         _lib.mfma_probe_run.restype = ctypes.c_int
+        _lib.unit_probe_run.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32,
+                                        ctypes.c_void_p, ctypes.c_void_p]
+        _lib.unit_probe_run.restype = ctypes.c_int
     return _lib
 
 
@@ -45,3 +49,19 @@ def status(iters: int, workgroups: int, sink_ptr) -> int:
     """The raw return code for the given arguments (argument checks only: the
     rejected cases launch nothing)."""
     return int(_load().mfma_probe_run(int(iters), int(workgroups), sink_ptr, None))
+
+
+UNIT_KINDS = {"exp": 0, "fma": 1, "lds": 2}
+
+
+def run_unit(kind: str, iters: int, workgroups: int, sink, stream=None) -> None:
+    """Enqueue one unit probe ("exp", "fma": 16 instructions per wave and
+    iteration; "lds": 32 ds_read_b128 per wave and iteration)."""
+    import torch
+    if sink.numel() < int(workgroups) * 256 or sink.dtype != torch.float32 or not sink.is_cuda:
+        raise ValueError("sink must be a float32 cuda tensor of workgroups * 256 elements")
+    st = stream if stream is not None else torch.cuda.current_stream(sink.device)
+    rc = _load().unit_probe_run(UNIT_KINDS[kind], int(iters), int(workgroups), sink.data_ptr(),
+                                st.cuda_stream)
+    if rc != 0:
+        raise RuntimeError(f"unit probe {kind} failed with status {rc}")
