@@ -343,6 +343,15 @@ def test_mfma_probe_is_outside_the_abi(lib):
     assert probe.status(10, 0, P) == E_INVALID
     assert probe.status(10, (1 << 20) + 1, P) == E_INVALID
     assert probe.status(10, 4, None) == E_INVALID
+    # the unit probes beside it reject bad arguments before any launch
+    u = probe._load().unit_probe_run
+    assert not hasattr(lib, "unit_probe_run")
+    assert u(3, 10, 4, P, None) == E_INVALID     # no such probe
+    assert u(-1, 10, 4, P, None) == E_INVALID
+    assert u(0, 0, 4, P, None) == E_INVALID      # iters < 1
+    assert u(2, 10, 0, P, None) == E_INVALID     # no workgroups
+    assert u(1, 10, (1 << 20) + 1, P, None) == E_INVALID
+    assert u(1, 10, 4, None, None) == E_INVALID  # no sink
 
 
 def test_row_order_and_ordered_attention_rejected(lib):
