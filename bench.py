@@ -680,6 +680,24 @@ def main(argv=None) -> int:
         c = rec["chunked_attention"]
         log(f"[bench] shard-by-shard: {c['chunks']} chunks {c['chunked_ms']:.3f} ms vs "
             f"{c['unchunked_f32_out_ms']:.3f} ms unchunked; merge {c['merge']['GBps']:.0f} GB/s")
+    if a.extensions and flush is not None:
+        # The gather call alone right after the cache flush, so that none of
+        # K and V can come from the Infinity Cache or the L2s (in the step,
+        # pooling has just streamed K).
+        gms = []
+        for _ in range(10):
+            cold()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            sp.sparsp_demand_union_gather(g, bufs["mask"], K, V, cap, out=packed, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            gms.append(e0.elapsed_time(e1))
+        g_ms = float(np.median(gms))
+        rec["gather_cold"] = {"call_ms_median": g_ms, "GBps": gbytes / (g_ms * 1e-3) / 1e9,
+                              "frac_of_hbm_peak": gbytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS}
+        log(f"[bench] gather alone after a cache flush: {g_ms:.4f} ms = "
+            f"{rec['gather_cold']['GBps']:.0f} GB/s")
     if a.extensions and wl.dtype == "bf16":
         packed["_K"], packed["_V"] = K, V
         rec["cdf_selection"] = measure_cdf(sp, g, wl, Q, bufs, packed, stream)
